@@ -1,0 +1,252 @@
+#!/usr/bin/env python3
+"""Batch-1 gated early-exit decode benchmark on one MI355X.
+
+Workload: the 1.5B-shaped decoder (28 layers, H=1536, 12 query / 2 KV heads
+of 128, SwiGLU F=8960, V=151936, tied embeddings, bf16 weights with fp32
+accumulation), readout at layer 14, a 512-token random prompt, then decode
+steps. The threshold tau is calibrated on the GPU (ee_calibrate_threshold)
+from 16 seeded 512-token prompts x 128 full-depth steps to target exit rates
+0.5 (the headline `value`), 0 and 0.96; the ungated model is timed too.
+
+A step is one decode step (one token) through the whole gated path. W
+warm-up steps run first, then exactly K steps are timed in one ee_decode_n
+call (one persistent kernel launch), bracketed by device synchronisation.
+Weights and prompt are resident in HBM before timing starts.
+
+Output: one JSON line on stdout (progress goes to stderr).
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "batch-1 decode tokens/sec at exit rate r; achieved HBM GB/s vs peak"
+PEAK_HBM_GBS = 8000.0
+PROMPT = 512
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def step_bytes(cfg, exit_layer, T, exited, gated):
+    """Algorithmic HBM bytes of one decode step attending to T positions:
+    weights read once, cache entries read and written. Activations (a few
+    KB) and norm gains are left out."""
+    es = cfg.wbytes
+    H, K, D, V, L = cfg.hidden, cfg.n_kv_heads, cfg.head_dim, cfg.vocab, cfg.n_layers
+    layer = cfg.layer_params * es
+    kv_read = 2 * K * D * es * T
+    kv_write = 2 * K * D * es
+    E = V * H * es
+    readout = H * H * es + H * 4
+    if not gated:
+        return L * (layer + kv_read + kv_write) + E
+    if exited:
+        fill = (L - exit_layer) * (2 * K * D * H * es + kv_write)
+        return exit_layer * (layer + kv_read + kv_write) + readout + E + fill
+    return L * (layer + kv_read + kv_write) + readout + 2 * E
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("ee_kernels.hip", "ee_internal.h"):
+        with open(os.path.join(ROOT, "paper_2609_14144_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, n_steps_expected):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, if
+    they were taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return rec
+
+
+def run_condition(e, cfg, tau, exit_layer, prompt, warmup, steps):
+    import torch
+    e.ee_reset()
+    e.ee_prefill(prompt)
+    if warmup:
+        e.ee_decode_n(tau, exit_layer, warmup)
+    pos0 = e.ee_position()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    tok, ex, conf = e.ee_decode_n(tau, exit_layer, steps)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kernel_ms = e.ee_last_decode_ms()
+    gated = exit_layer > 0
+    nbytes = sum(step_bytes(cfg, exit_layer, pos0 + i + 1, bool(ex[i]), gated) for i in range(steps))
+    wall = t1 - t0
+    return {
+        "tau": None if math.isinf(tau) else float(tau),
+        "exit_layer": exit_layer,
+        "realised_exit_rate": float(ex.mean()),
+        "tokens_per_s": steps / wall,
+        "ms_per_step": 1e3 * wall / steps,
+        "kernel_ms": kernel_ms,
+        "kernel_tokens_per_s": steps / (kernel_ms * 1e-3),
+        "algorithmic_bytes": nbytes,
+        "achieved_GBs": nbytes / (kernel_ms * 1e-3) / 1e9,
+    }
+
+
+def cpu_baseline(cfg, w, prompt, tau, exit_layer, seconds):
+    """The CPU oracle (fp64 numpy) on a bounded sample of the same workload."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    o = oracle.OracleDecoder(cfg, w, PROMPT + 256)
+    t = time.perf_counter()
+    tok = o.prefill(prompt)
+    prefill_s = time.perf_counter() - t
+    n = 0
+    exits = 0
+    t = time.perf_counter()
+    while True:
+        r = o.decode_step(tok, tau, exit_layer)
+        tok = r.token
+        exits += r.exited
+        n += 1
+        el = time.perf_counter() - t
+        if (el >= seconds and n >= 4) or n >= 256:
+            break
+    return {"value": n / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"fp64 numpy oracle: prefill of the {PROMPT}-token prompt "
+                       f"({prefill_s:.1f} s, untimed), then the first {n} gated decode steps "
+                       f"at the headline tau (exit rate {exits / n:.2f}) on the host cores")}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=256)
+    ap.add_argument("--warmup", type=int, default=32)
+    ap.add_argument("--config", default="d1p5b")
+    ap.add_argument("--exit-layer", type=int, default=None, help="default: half depth")
+    ap.add_argument("--cal-prompts", type=int, default=16)
+    ap.add_argument("--cal-gen", type=int, default=128)
+    ap.add_argument("--program", choices=["persistent", "per_op"], default="persistent")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the batch-1 decode "
+              "step runs on a single MI355X, and multi-GPU runs are not part of this build.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import synth
+    from paper_2609_14144_amd import EE_CAL_EXIT_RATE, Engine
+
+    if not torch.cuda.is_available():
+        log("no GPU visible")
+        sys.exit(1)
+    cfg = synth.get_config(args.config)
+    Le = args.exit_layer or cfg.n_layers // 2
+    if Le not in cfg.readout_layers:
+        cfg = cfg.with_readouts(tuple(sorted(set(cfg.readout_layers) | {Le})))
+    t = time.perf_counter()
+    w = synth.generate_weights(cfg)
+    log(f"weights generated in {time.perf_counter() - t:.1f}s")
+    max_seq = PROMPT + max(args.warmup + args.steps, args.cal_gen) + 8
+    e = Engine(cfg, max_seq)
+    e.ee_load_weights(w)
+    e.ee_set_persistent(args.program == "persistent")
+    log("weights resident on the GPU")
+
+    cal = [synth.prompts(cfg, 200 + i, PROMPT) for i in range(args.cal_prompts)]
+    rates = [0.5] if args.no_sweep else [0.5, 0.0, 0.96]
+    taus = {}
+    t = time.perf_counter()
+    for r in rates:
+        taus[r] = e.ee_calibrate_threshold(cal, args.cal_gen, Le, EE_CAL_EXIT_RATE, r)
+    log(f"calibrated tau {taus} in {time.perf_counter() - t:.1f}s")
+
+    prompt = synth.prompts(cfg, 1, PROMPT)
+    # warm the code path once on another prompt
+    e.ee_reset()
+    e.ee_prefill(synth.prompts(cfg, 2, PROMPT))
+    e.ee_decode_n(taus[0.5], Le, 8)
+
+    results = {}
+    for r in rates:
+        results[f"r{r:g}"] = run_condition(e, cfg, taus[r], Le, prompt, args.warmup, args.steps)
+        log(f"target exit rate {r}: {results[f'r{r:g}']}")
+    if not args.no_sweep:
+        results["ungated"] = run_condition(e, cfg, math.inf, 0, prompt, args.warmup, args.steps)
+        log(f"ungated: {results['ungated']}")
+    head = results["r0.5"]
+
+    kname = "k_decode_persistent" if args.program == "persistent" else "per_op"
+    per_launch = head["algorithmic_bytes"]
+    traffic = None
+    rec = measured_traffic(kname, args.steps)
+    if rec is not None:
+        traffic = rec.get("hbm_bytes_per_launch")
+    roofline = {"bound": "hbm", "achieved": head["achieved_GBs"], "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": head["achieved_GBs"] / PEAK_HBM_GBS, "traffic": traffic,
+                "kernel": kname, "algorithmic_bytes_per_launch": per_launch,
+                "launch_ms": head["kernel_ms"]}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        t = time.perf_counter()
+        cpu = cpu_baseline(cfg, w, prompt, taus[0.5], Le, args.cpu_seconds)
+        log(f"cpu baseline {cpu} ({time.perf_counter() - t:.1f}s incl. setup)")
+
+    out = {
+        "metric": METRIC,
+        "value": head["tokens_per_s"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 weights, f32 accumulate",
+        "data": "synthetic (seeded random weights N(0,0.02) and uniform random prompts)",
+        "config": {
+            "workload": (f"1.5B-shaped decoder: {cfg.n_layers} layers, H={cfg.hidden}, "
+                         f"{cfg.n_q_heads}/{cfg.n_kv_heads} heads of {cfg.head_dim}, F={cfg.ffn}, "
+                         f"V={cfg.vocab}, bf16; readout at layer {Le}; {PROMPT}-token prompt, "
+                         f"{args.warmup} warm-up + {args.steps} timed decode steps, batch 1; tau "
+                         f"calibrated on the GPU to target exit rate 0.5"),
+            "exit_layer": Le,
+            "target_exit_rate": 0.5,
+            "realised_exit_rate": head["realised_exit_rate"],
+            "tau": head["tau"],
+            "program": args.program,
+        },
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "sweep": results,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

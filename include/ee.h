@@ -1,0 +1,217 @@
+/*
+ * ee.h - C ABI of the gated early-exit decode library for MI355X (gfx950).
+ *
+ * One batch-1 decode step (the method of "One Size Does Not Fit All: Setting
+ * Inference Depth from the Questions a Deployment Actually Asks", Section 4,
+ * step five) runs the decoder layers up to an exit layer L_e, applies the
+ * readout (a square matrix plus an offset whose result passes through the
+ * model's own final RMSNorm and tied unembedding; Section 2 "Readout, or
+ * lens", Appendix B), tests the readout's softmax max-probability against a
+ * threshold tau (Section 2 "Confidence gate"), and then either emits the
+ * readout's token, supplying the skipped layers' key/value cache entries by
+ * projecting the exit-layer state through those layers' key and value
+ * matrices (Section 4, step five), or runs the remaining layers and emits the
+ * full model's token. Decoding is greedy.
+ *
+ * Conventions shared by every entry point
+ *   - Return value: EE_OK (0) on success, a negative EE_E* code otherwise.
+ *     ee_last_error() then describes the failure. No C++ exception crosses
+ *     the ABI. After an error the context remains valid; ee_reset() restores
+ *     a clean sequence state.
+ *   - Host pointers are plain CPU memory owned by the caller. Device pointers
+ *     (where an argument says so) are HIP device memory on the context's
+ *     device, owned by the caller.
+ *   - The library owns everything it allocates (repacked weights, KV pages,
+ *     workspace) and frees it in ee_destroy().
+ *   - A context is bound to one HIP stream and is not thread-safe.
+ *   - exit_layer counts the decoder layers run before the readout, 1..L. The
+ *     value 0 selects the plain ungated model (no readout, no gate): the
+ *     baseline.
+ *   - The gate exits iff conf > tau, compared in fp32. tau = +inf never exits;
+ *     tau <= 0 always exits (conf >= 1/V > 0). tau = NaN is EE_EINVAL.
+ *   - conf is the readout's max softmax probability, also on fallback steps;
+ *     for the ungated model it is the full head's.
+ *   - Argmax ties go to the lowest token id.
+ */
+#ifndef EE_H
+#define EE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  EE_OK = 0,
+  EE_EINVAL = -1,    /* bad argument: shape, name, size, exit layer without readout, NaN tau */
+  EE_ESTATE = -2,    /* call not valid in this state (weights missing, decode before prefill) */
+  EE_ENOMEM = -3,    /* device or host allocation failed */
+  EE_EHIP = -4,      /* HIP runtime error */
+  EE_ECAPACITY = -5, /* KV cache capacity (max_seq) would be exceeded */
+  EE_EDEVICE = -6    /* the device reported an error (bounded wait timed out, bad token) */
+};
+
+enum { EE_F32 = 0, EE_BF16 = 1 }; /* storage type of matrices and KV cache */
+
+enum {
+  EE_CAL_EXIT_RATE = 0, /* tau so that a replay exits round(target*n) of n tokens */
+  EE_CAL_MEDIAN = 1     /* tau = median readout confidence (target ignored) */
+};
+
+typedef struct ee_config {
+  int32_t n_layers;   /* L */
+  int32_t hidden;     /* H, multiple of 8 */
+  int32_t n_q_heads;  /* A */
+  int32_t n_kv_heads; /* K, A % K == 0, A/K <= 8 */
+  int32_t head_dim;   /* D, even, D*elem_size a multiple of 16, D <= 256 */
+  int32_t ffn;        /* F, multiple of 8 */
+  int32_t vocab;      /* V */
+  float rope_base;    /* rotate-half RoPE base */
+  float rms_eps;      /* RMSNorm epsilon */
+  int32_t wdtype;     /* EE_F32 or EE_BF16 */
+  int32_t max_seq;    /* KV capacity in positions */
+  int32_t page_size;  /* positions per KV page, power of two */
+} ee_config;
+
+/* One named weight tensor. Matrices are canonical [out, in] row-major in the
+ * configured storage type (fp32, or bf16 bit patterns); gains and offsets are
+ * always fp32. ptr is host memory unless on_device != 0. Names:
+ *   embed [V,H]; layers.{l}.attn_norm [H]; layers.{l}.wq [A*D,H];
+ *   layers.{l}.wk [K*D,H]; layers.{l}.wv [K*D,H]; layers.{l}.wo [H,A*D];
+ *   layers.{l}.mlp_norm [H]; layers.{l}.w_gate [F,H]; layers.{l}.w_up [F,H];
+ *   layers.{l}.w_down [H,F]; final_norm [H]; readout.{L_e}.w [H,H];
+ *   readout.{L_e}.b [H]   (l is 0-based, L_e is 1..L). */
+typedef struct ee_tensor {
+  const char* name;
+  const void* ptr;
+  int64_t nbytes;
+  int32_t on_device;
+} ee_tensor;
+
+/* Per-step debug record filled by ee_decode_step_ex. Array pointers are host
+ * memory and may be NULL; arrays a step does not produce are left untouched
+ * (h_final and logits_full on exited steps, readout fields when ungated). */
+typedef struct ee_debug {
+  float* h_exit;          /* [H] residual stream after layer L_e */
+  float* h_final;         /* [H] residual stream after layer L */
+  float* logits_readout;  /* [V] readout logits */
+  float* logits_full;     /* [V] full-head logits */
+  int32_t token;          /* emitted token */
+  int32_t exited;         /* branch taken */
+  int32_t would_exit;     /* gate decision (conf > tau) before forcing */
+  int32_t readout_token;  /* readout argmax, -1 when ungated */
+  int32_t full_token;     /* full-head argmax, -1 when the upper layers were skipped */
+  float conf;             /* readout max-probability (full head's when ungated) */
+  float conf_full;        /* full head max-probability, NaN when skipped */
+} ee_debug;
+
+typedef struct ee_ctx ee_ctx;
+
+/* Create a context on the current HIP device. hip_stream is a hipStream_t
+ * (for instance torch's current stream) or NULL for a library-owned stream.
+ * Allocates the KV pool for max_seq positions and the workspace.
+ * Errors: EE_EINVAL (shape constraints above), EE_ENOMEM, EE_EHIP. */
+int ee_create(const ee_config* cfg, void* hip_stream, ee_ctx** out);
+
+/* Copy (and repack for the kernels' layouts) weights into library memory.
+ * May be called several times; a later tensor of the same name replaces the
+ * earlier one. Decoding needs every non-readout tensor; gated decoding at
+ * exit layer L_e also needs readout.{L_e}.w and .b. Synchronous.
+ * Errors: EE_EINVAL (unknown name, wrong nbytes), EE_ENOMEM, EE_EHIP. */
+int ee_load_weights(ee_ctx* ctx, const ee_tensor* tensors, int32_t n_tensors);
+
+/* Prompt pass at full depth, ungated, over positions pos..pos+n-1 (host token
+ * ids in [0,V)). Writes every layer's KV entries and returns in
+ * *out_first_token the full head's argmax at the last prompt position, which
+ * becomes the next decode step's input. Synchronous.
+ * Errors: EE_ESTATE (weights incomplete), EE_EINVAL (n <= 0, bad token),
+ * EE_ECAPACITY, EE_EHIP, EE_EDEVICE. */
+int ee_prefill(ee_ctx* ctx, const int32_t* tokens, int32_t n, int32_t* out_first_token);
+
+/* One gated decode step on the last emitted token; syncs once.
+ * Outputs (host, any may be NULL): emitted token, exited flag, conf.
+ * Errors: EE_ESTATE (no prefill yet / weights incomplete), EE_EINVAL
+ * (exit_layer out of 0..L or without a loaded readout, NaN tau),
+ * EE_ECAPACITY, EE_EHIP, EE_EDEVICE. */
+int ee_decode_step(ee_ctx* ctx, float tau, int32_t exit_layer,
+                   int32_t* out_token, int32_t* out_exited, float* out_conf);
+
+/* n gated decode steps enqueued as one device program; each step's input is
+ * the previous step's output token, read on the device, so the host never
+ * waits per token. One sync at the end. tokens/exited/conf are host arrays of
+ * n entries (any may be NULL). Errors as ee_decode_step, plus EE_EINVAL for
+ * n <= 0. */
+int ee_decode_n(ee_ctx* ctx, float tau, int32_t exit_layer, int32_t n,
+                int32_t* tokens, int32_t* exited, float* conf);
+
+/* ee_decode_n with optional imposed inputs (host arrays of n, may be NULL):
+ * force_tokens[i] replaces step i's input token (teacher forcing; the first
+ * step may then run without a prior prefill output), force_exit[i] is -1
+ * (use the gate), 0 (never exit) or 1 (always exit); imposed exit decisions
+ * are the paper's timing method (Appendix C). would_exit[i] receives the gate's
+ * own decision. Errors as ee_decode_n, plus EE_EINVAL for bad forced values. */
+int ee_decode_n_ex(ee_ctx* ctx, float tau, int32_t exit_layer, int32_t n,
+                   const int32_t* force_tokens, const int32_t* force_exit,
+                   int32_t* tokens, int32_t* exited, float* conf, int32_t* would_exit);
+
+/* One step with an optional input token (-1 = last emitted), an optional
+ * imposed branch (-1 gate, 0 never exit, 1 always exit) and a debug record
+ * (may be NULL). Test hook; runs the same device program as ee_decode_n. */
+int ee_decode_step_ex(ee_ctx* ctx, float tau, int32_t exit_layer, int32_t input_token,
+                      int32_t force_exit, ee_debug* dbg);
+
+/* Calibrate tau on the device (Section 4, step four): for each prompt,
+ * reset, prefill, then n_gen steps at tau = +inf (full depth, readout
+ * computed), recording the readout confidences. EE_CAL_EXIT_RATE: with the n
+ * recorded values sorted ascending c_1..c_n and k = floor(target*n + 1/2),
+ * tau = c_(n-k) (+inf for k = 0, -inf for k = n). EE_CAL_MEDIAN: the median.
+ * prompts holds the prompts back to back (host), prompt_lens their lengths.
+ * Leaves the context reset. Errors: EE_EINVAL, EE_ESTATE, EE_ECAPACITY,
+ * EE_EHIP, EE_EDEVICE. */
+int ee_calibrate_threshold(ee_ctx* ctx, const int32_t* prompts, const int32_t* prompt_lens,
+                           int32_t n_prompts, int32_t n_gen, int32_t exit_layer,
+                           int32_t mode, float target, float* out_tau);
+
+/* Replace the offset b (H fp32) of the readout at exit_layer, asynchronously
+ * on the context's stream (no sync): later steps enqueued on the stream see
+ * it. Errors: EE_EINVAL (no readout at that layer), EE_EHIP. */
+int ee_set_readout_bias(ee_ctx* ctx, int32_t exit_layer, const float* b, int32_t on_device);
+
+/* Evaluate one head on a caller vector x (H fp32, host): layer 0 = the full
+ * head (final RMSNorm + unembedding), layer L_e = the readout at L_e followed
+ * by the full head. Runs the decode step's head kernel. Outputs (any may be
+ * NULL): argmax token, max-probability, logits [V] (host). Test hook. */
+int ee_head_eval(ee_ctx* ctx, int32_t readout_layer, const float* x,
+                 int32_t* out_token, float* out_conf, float* out_logits);
+
+/* Copy the cache entries of (layer, position) as fp32 into k_out and v_out
+ * (host, K*D each, [kv_head][d], post-RoPE keys). Test hook.
+ * Errors: EE_EINVAL (layer or pos out of range / not yet written). */
+int ee_read_kv(ee_ctx* ctx, int32_t layer, int32_t pos, float* k_out, float* v_out);
+
+/* Select the device program used for decoding: 1 = one persistent
+ * cooperative kernel per call (default), 0 = one kernel per operation. */
+int ee_set_persistent(ee_ctx* ctx, int32_t on);
+
+/* Device time in milliseconds of the most recent ee_decode_n/_ex call's
+ * kernels, measured with HIP events on the context's stream. */
+int ee_last_decode_ms(ee_ctx* ctx, float* out_ms);
+
+/* Sequence position (number of cached positions). */
+int32_t ee_position(const ee_ctx* ctx);
+
+/* Drop the KV cache contents and position, keep weights. */
+int ee_reset(ee_ctx* ctx);
+
+/* Message of the most recent error on ctx (empty string if none). With
+ * ctx == NULL: the message of this thread's most recent ee_create failure. */
+const char* ee_last_error(const ee_ctx* ctx);
+
+void ee_destroy(ee_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EE_H */

@@ -237,8 +237,8 @@ class OracleDecoder:
             m = rmsnorm(H, lw["g_mlp"], c.rms_eps)
             H = H + (silu(m @ lw["wg"].T) * (m @ lw["wu"].T)) @ lw["wd"].T
         self.pos = T
-        j, _, _ = head_stats(self.full_logits(H[-1]))
-        return j
+        self.last_prefill_stats = head_stats(self.full_logits(H[-1]))  # (token, conf, gap)
+        return self.last_prefill_stats[0]
 
     def generate(self, first_token: int, tau: float, exit_layer: int, n: int,
                  force_tokens=None, force_exit=None, keep_logits=False):

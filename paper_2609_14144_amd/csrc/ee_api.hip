@@ -1,0 +1,812 @@
+// C ABI of the gated early-exit decode library: context, weight loading and
+// repacking, paged KV allocation, step launching, calibration, test hooks.
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <algorithm>
+#include <map>
+#include <new>
+#include <random>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "ee.h"
+#include "ee_internal.h"
+
+using ee::DevParams;
+
+struct ee_ctx {
+  ee_config cfg{};
+  int wbf16 = 0;
+  size_t esz = 4;
+  hipStream_t stream = nullptr;
+  bool own_stream = false;
+  int device = 0;
+  int n_cu = 0;
+
+  void* embed = nullptr;
+  std::vector<void*> wqkv, wo, wgu, wd;
+  std::vector<float*> g_attn, g_mlp;
+  float* g_final = nullptr;
+  std::map<int, std::pair<void*, float*>> readout;
+  ee::LayerW* d_layers = nullptr;
+
+  void* kpool = nullptr;
+  void* vpool = nullptr;
+  int64_t layer_stride = 0;
+  int n_pages = 0;
+  int32_t* d_block_table = nullptr;
+  int32_t* h_block_table = nullptr;  // pinned
+  int pages_mapped = 0;
+  std::vector<int32_t> free_pages;
+
+  float* d_cos = nullptr;
+  float* d_sin = nullptr;
+  float *d_h = nullptr, *d_hexit = nullptr, *d_z = nullptr, *d_q = nullptr, *d_o = nullptr,
+        *d_a = nullptr;
+  float* d_attn_part = nullptr;
+  int max_splits = 0;
+  float* d_head_part = nullptr;
+  int max_parts = 0;
+  ee::Counters* d_counters = nullptr;
+  ee::StepCtl* d_ctl = nullptr;
+
+  int ring_cap = 0;
+  int32_t *d_ring_tok = nullptr, *d_ring_exit = nullptr, *d_ring_would = nullptr;
+  float* d_ring_conf = nullptr;
+  int force_cap = 0;
+  int32_t *d_force_tok = nullptr, *d_force_exit = nullptr;
+  float *d_dbg_r = nullptr, *d_dbg_f = nullptr, *d_x = nullptr;
+
+  std::set<std::string> loaded;
+  int pos = 0;
+  bool have_next = false;
+  bool persistent = true;
+  int head_wgs = 0;
+  int nwg_persistent = 0;
+  size_t lds = 0;
+  hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  float last_ms = 0.f;
+  std::string err;
+};
+
+namespace {
+
+thread_local std::string g_create_err;  // last ee_create failure (no context exists)
+
+int fail(ee_ctx* c, int code, const std::string& msg) {
+  if (c) c->err = msg;
+  return code;
+}
+
+int hip_fail(ee_ctx* c, hipError_t e, const char* what) {
+  return fail(c, EE_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define HIPCHK(ctx, call)                                     \
+  do {                                                        \
+    hipError_t e_ = (call);                                   \
+    if (e_ != hipSuccess) return hip_fail((ctx), e_, #call);  \
+  } while (0)
+
+template <typename T>
+int dalloc(ee_ctx* c, T** p, size_t bytes) {
+  void* q = nullptr;
+  if (hipMalloc(&q, bytes ? bytes : 16) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(c, EE_ENOMEM, "hipMalloc of " + std::to_string(bytes) + " bytes failed");
+  }
+  const hipError_t e = hipMemset(q, 0, bytes ? bytes : 16);
+  if (e != hipSuccess) {
+    (void)hipFree(q);
+    return hip_fail(c, e, "hipMemset");
+  }
+  *p = static_cast<T*>(q);
+  return EE_OK;
+}
+
+void dfree(void* p) {
+  if (p) (void)hipFree(p);
+}
+
+int elems_per_chunk(const ee_ctx* c) { return c->wbf16 ? 8 : 4; }
+
+bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+
+int validate_config(const ee_config* g, std::string& why) {
+  const int N = g->wdtype == EE_BF16 ? 8 : 4;
+  if (g->wdtype != EE_F32 && g->wdtype != EE_BF16) { why = "wdtype must be EE_F32 or EE_BF16"; return 0; }
+  if (g->n_layers < 1 || g->n_layers > 512) { why = "n_layers out of range"; return 0; }
+  if (g->hidden < 8 || g->hidden % 8) { why = "hidden must be a positive multiple of 8"; return 0; }
+  if (g->ffn < 8 || g->ffn % 8) { why = "ffn must be a positive multiple of 8"; return 0; }
+  if (g->n_kv_heads < 1 || g->n_kv_heads > 16) { why = "n_kv_heads must be 1..16"; return 0; }
+  if (g->n_q_heads < 1 || g->n_q_heads % g->n_kv_heads) { why = "n_q_heads must be a multiple of n_kv_heads"; return 0; }
+  if (g->n_q_heads / g->n_kv_heads > ee::kMaxGroup) { why = "more than 8 query heads per kv head"; return 0; }
+  if (g->head_dim < 2 || g->head_dim > ee::kMaxHeadDim || g->head_dim % N) {
+    why = "head_dim must be a multiple of 16 bytes of storage and at most 256"; return 0;
+  }
+  if (64 % (g->head_dim / N)) { why = "head_dim / elems-per-16-bytes must divide 64"; return 0; }
+  if ((g->head_dim * (g->wdtype == EE_BF16 ? 2 : 4)) % 128) {
+    why = "a KV row (head_dim elements) must fill whole 128-byte lines"; return 0;
+  }
+  if (g->vocab < 2) { why = "vocab must be >= 2"; return 0; }
+  if (g->max_seq < 1) { why = "max_seq must be >= 1"; return 0; }
+  if (!is_pow2(g->page_size)) { why = "page_size must be a power of two"; return 0; }
+  if (!(g->rms_eps > 0.f) || !(g->rope_base > 0.f)) { why = "rms_eps and rope_base must be positive"; return 0; }
+  return 1;
+}
+
+DevParams make_params(const ee_ctx* c, float tau, int exit_layer) {
+  const ee_config& g = c->cfg;
+  DevParams p{};
+  p.L = g.n_layers; p.H = g.hidden; p.A = g.n_q_heads; p.K = g.n_kv_heads; p.D = g.head_dim;
+  p.F = g.ffn; p.V = g.vocab; p.G = g.n_q_heads / g.n_kv_heads;
+  p.qkv_rows = (p.A + 2 * p.K) * p.D;
+  p.eps = g.rms_eps;
+  p.attn_scale = static_cast<float>(1.0 / sqrt(static_cast<double>(p.D)));
+  p.tau = tau;
+  p.exit_layer = exit_layer;
+  p.page_size = g.page_size;
+  int sh = 0;
+  while ((1 << sh) < g.page_size) ++sh;
+  p.page_shift = sh;
+  p.embed = c->embed;
+  p.layers = c->d_layers;
+  p.g_final = c->g_final;
+  if (exit_layer > 0) {
+    auto it = c->readout.find(exit_layer);
+    p.ro_w = it->second.first;
+    p.ro_b = it->second.second;
+  }
+  p.kpool = c->kpool; p.vpool = c->vpool; p.layer_stride = c->layer_stride;
+  p.block_table = c->d_block_table;
+  p.rope_cos = c->d_cos; p.rope_sin = c->d_sin;
+  p.h = c->d_h; p.h_exit = c->d_hexit; p.z = c->d_z; p.q = c->d_q; p.o = c->d_o; p.a = c->d_a;
+  p.attn_part = c->d_attn_part; p.max_splits = c->max_splits;
+  p.head_part = c->d_head_part; p.max_parts = c->max_parts;
+  p.counters = c->d_counters; p.ctl = c->d_ctl;
+  return p;
+}
+
+int ensure_pages(ee_ctx* c, int pos_end) {
+  if (pos_end > c->cfg.max_seq)
+    return fail(c, EE_ECAPACITY, "KV capacity exceeded: need " + std::to_string(pos_end) +
+                                     " positions, max_seq " + std::to_string(c->cfg.max_seq));
+  const int need = (pos_end + c->cfg.page_size - 1) / c->cfg.page_size;
+  const int first = c->pages_mapped;
+  while (c->pages_mapped < need) {
+    c->h_block_table[c->pages_mapped++] = c->free_pages.back();
+    c->free_pages.pop_back();
+  }
+  if (c->pages_mapped > first)
+    HIPCHK(c, hipMemcpyAsync(c->d_block_table + first, c->h_block_table + first,
+                             sizeof(int32_t) * (c->pages_mapped - first), hipMemcpyHostToDevice,
+                             c->stream));
+  return EE_OK;
+}
+
+void reset_pages(ee_ctx* c) {
+  c->pages_mapped = 0;
+  c->free_pages.resize(c->n_pages);
+  for (int i = 0; i < c->n_pages; ++i) c->free_pages[i] = i;
+  // A fixed scrambled order: physical page order differs from logical order.
+  std::mt19937 rng(12345u);
+  std::shuffle(c->free_pages.begin(), c->free_pages.end(), rng);
+}
+
+int ensure_ring(ee_ctx* c, int n) {
+  if (n <= c->ring_cap) return EE_OK;
+  dfree(c->d_ring_tok); dfree(c->d_ring_exit); dfree(c->d_ring_would); dfree(c->d_ring_conf);
+  c->d_ring_tok = c->d_ring_exit = c->d_ring_would = nullptr;
+  c->d_ring_conf = nullptr;
+  c->ring_cap = 0;
+  int r;
+  if ((r = dalloc(c, &c->d_ring_tok, sizeof(int32_t) * n))) return r;
+  if ((r = dalloc(c, &c->d_ring_exit, sizeof(int32_t) * n))) return r;
+  if ((r = dalloc(c, &c->d_ring_would, sizeof(int32_t) * n))) return r;
+  if ((r = dalloc(c, &c->d_ring_conf, sizeof(float) * n))) return r;
+  c->ring_cap = n;
+  return EE_OK;
+}
+
+int ensure_force(ee_ctx* c, int n) {
+  if (n <= c->force_cap) return EE_OK;
+  dfree(c->d_force_tok); dfree(c->d_force_exit);
+  c->d_force_tok = c->d_force_exit = nullptr;
+  c->force_cap = 0;
+  int r;
+  if ((r = dalloc(c, &c->d_force_tok, sizeof(int32_t) * n))) return r;
+  if ((r = dalloc(c, &c->d_force_exit, sizeof(int32_t) * n))) return r;
+  c->force_cap = n;
+  return EE_OK;
+}
+
+bool weights_ready(const ee_ctx* c) {
+  return c->loaded.size() >= static_cast<size_t>(2 + 9 * c->cfg.n_layers) &&
+         c->loaded.count("embed") && c->loaded.count("final_norm");
+}
+
+int check_gate_args(ee_ctx* c, float tau, int exit_layer) {
+  if (isnan(tau)) return fail(c, EE_EINVAL, "tau is NaN");
+  if (exit_layer < 0 || exit_layer > c->cfg.n_layers)
+    return fail(c, EE_EINVAL, "exit_layer must be in 0..n_layers");
+  if (exit_layer > 0 && !c->readout.count(exit_layer))
+    return fail(c, EE_EINVAL, "no readout loaded at layer " + std::to_string(exit_layer));
+  if (!weights_ready(c)) return fail(c, EE_ESTATE, "weights not fully loaded");
+  return EE_OK;
+}
+
+// Launch n steps (decode, or prompt positions when prefill) and wait.
+int run_steps(ee_ctx* c, float tau, int exit_layer, int n, const int32_t* d_force_tok,
+              const int32_t* d_force_exit, bool prefill, bool debug) {
+  int r;
+  if ((r = ensure_ring(c, n))) return r;
+  if ((r = ensure_pages(c, c->pos + n))) return r;
+  DevParams p = make_params(c, tau, prefill ? 0 : exit_layer);
+  p.ring_tok = c->d_ring_tok; p.ring_exit = c->d_ring_exit;
+  p.ring_would = c->d_ring_would; p.ring_conf = c->d_ring_conf;
+  p.force_tok = d_force_tok;
+  p.force_exit = d_force_exit;
+  if (debug) {
+    p.dbg_logits_r = c->d_dbg_r;
+    p.dbg_logits_f = c->d_dbg_f;
+  }
+  // Clear the step record except next_token, the first step's input.
+  HIPCHK(c, hipMemsetAsync(reinterpret_cast<char*>(c->d_ctl) + offsetof(ee::StepCtl, exited), 0,
+                           offsetof(ee::StepCtl, pad) - offsetof(ee::StepCtl, exited), c->stream));
+  HIPCHK(c, hipEventRecord(c->ev0, c->stream));
+  hipError_t e;
+  const bool pers = c->persistent && c->nwg_persistent > 0;
+  if (prefill) {
+    e = pers ? ee::launch_prefill_persistent(p, c->wbf16, c->pos, n, c->nwg_persistent, c->lds, c->stream)
+             : ee::launch_prefill_per_op(p, c->wbf16, c->pos, d_force_tok, n, c->head_wgs, c->stream);
+  } else {
+    e = pers ? ee::launch_decode_persistent(p, c->wbf16, c->pos, n, c->nwg_persistent, c->lds, c->stream)
+             : ee::launch_decode_per_op(p, c->wbf16, c->pos, n, c->head_wgs, c->stream);
+  }
+  if (e != hipSuccess) return hip_fail(c, e, "kernel launch");
+  HIPCHK(c, hipEventRecord(c->ev1, c->stream));
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  HIPCHK(c, hipEventElapsedTime(&c->last_ms, c->ev0, c->ev1));
+  ee::StepCtl ctl;
+  HIPCHK(c, hipMemcpy(&ctl, c->d_ctl, sizeof(ctl), hipMemcpyDeviceToHost));
+  if (ctl.error != ee::kErrNone || ctl.abort) {
+    c->have_next = false;
+    return fail(c, EE_EDEVICE, ctl.error == ee::kErrToken ? "device: token id out of range"
+                                                          : "device: bounded grid wait timed out");
+  }
+  c->pos += n;
+  c->have_next = true;
+  return EE_OK;
+}
+
+int copy_ring(ee_ctx* c, int n, int32_t* tokens, int32_t* exited, float* conf, int32_t* would) {
+  if (tokens) HIPCHK(c, hipMemcpy(tokens, c->d_ring_tok, sizeof(int32_t) * n, hipMemcpyDeviceToHost));
+  if (exited) HIPCHK(c, hipMemcpy(exited, c->d_ring_exit, sizeof(int32_t) * n, hipMemcpyDeviceToHost));
+  if (conf) HIPCHK(c, hipMemcpy(conf, c->d_ring_conf, sizeof(float) * n, hipMemcpyDeviceToHost));
+  if (would) HIPCHK(c, hipMemcpy(would, c->d_ring_would, sizeof(int32_t) * n, hipMemcpyDeviceToHost));
+  return EE_OK;
+}
+
+int upload_force(ee_ctx* c, int n, const int32_t* force_tokens, const int32_t* force_exit) {
+  int r;
+  if (!force_tokens && !force_exit) return EE_OK;
+  if ((r = ensure_force(c, n))) return r;
+  if (force_tokens) {
+    for (int i = 0; i < n; ++i)
+      if (force_tokens[i] < 0 || force_tokens[i] >= c->cfg.vocab)
+        return fail(c, EE_EINVAL, "force_tokens[" + std::to_string(i) + "] out of range");
+    HIPCHK(c, hipMemcpy(c->d_force_tok, force_tokens, sizeof(int32_t) * n, hipMemcpyHostToDevice));
+  }
+  if (force_exit) {
+    for (int i = 0; i < n; ++i)
+      if (force_exit[i] < -1 || force_exit[i] > 1)
+        return fail(c, EE_EINVAL, "force_exit values must be -1, 0 or 1");
+    HIPCHK(c, hipMemcpy(c->d_force_exit, force_exit, sizeof(int32_t) * n, hipMemcpyHostToDevice));
+  }
+  return EE_OK;
+}
+
+int decode_common(ee_ctx* c, float tau, int exit_layer, int n, const int32_t* force_tokens,
+                  const int32_t* force_exit, bool debug) {
+  int r;
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  if (n <= 0) return fail(c, EE_EINVAL, "n must be positive");
+  if ((r = check_gate_args(c, tau, exit_layer))) return r;
+  if (!force_tokens && !c->have_next)
+    return fail(c, EE_ESTATE, "no input token: run ee_prefill first (or force the input tokens)");
+  if ((r = upload_force(c, n, force_tokens, force_exit))) return r;
+  return run_steps(c, tau, exit_layer, n, force_tokens ? c->d_force_tok : nullptr,
+                   force_exit ? c->d_force_exit : nullptr, false, debug);
+}
+
+// Copy a matrix given in canonical layout into a row range of a repacked one.
+int copy_rows(ee_ctx* c, void* dst, size_t dst_pitch, const void* src, size_t src_pitch,
+              size_t row_bytes, size_t rows) {
+  HIPCHK(c, hipMemcpy2D(dst, dst_pitch, src, src_pitch, row_bytes, rows, hipMemcpyDefault));
+  return EE_OK;
+}
+
+// q or k heads: pair-interleave rows (i, i + D/2) of every head.
+int copy_rope_heads(ee_ctx* c, char* dst, const char* src, int heads) {
+  const int D = c->cfg.head_dim;
+  const size_t rb = static_cast<size_t>(c->cfg.hidden) * c->esz;
+  int r;
+  for (int h = 0; h < heads; ++h) {
+    char* d = dst + static_cast<size_t>(h) * D * rb;
+    const char* s = src + static_cast<size_t>(h) * D * rb;
+    if ((r = copy_rows(c, d, 2 * rb, s, rb, rb, D / 2))) return r;
+    if ((r = copy_rows(c, d + rb, 2 * rb, s + (D / 2) * rb, rb, rb, D / 2))) return r;
+  }
+  return EE_OK;
+}
+
+int load_one(ee_ctx* c, const ee_tensor& t) {
+  const ee_config& g = c->cfg;
+  const int64_t H = g.hidden, A = g.n_q_heads, K = g.n_kv_heads, D = g.head_dim, F = g.ffn,
+                V = g.vocab;
+  const int64_t es = static_cast<int64_t>(c->esz);
+  if (!t.name || !t.ptr) return fail(c, EE_EINVAL, "tensor with null name or pointer");
+  const std::string name(t.name);
+  auto need = [&](int64_t bytes) -> int {
+    if (t.nbytes != bytes)
+      return fail(c, EE_EINVAL, "tensor " + name + ": nbytes " + std::to_string(t.nbytes) +
+                                    ", expected " + std::to_string(bytes));
+    return EE_OK;
+  };
+  int r;
+  if (name == "embed") {
+    if ((r = need(V * H * es))) return r;
+    HIPCHK(c, hipMemcpy(c->embed, t.ptr, t.nbytes, hipMemcpyDefault));
+  } else if (name == "final_norm") {
+    if ((r = need(H * 4))) return r;
+    HIPCHK(c, hipMemcpy(c->g_final, t.ptr, t.nbytes, hipMemcpyDefault));
+  } else if (name.rfind("layers.", 0) == 0) {
+    const size_t dot = name.find('.', 7);
+    if (dot == std::string::npos) return fail(c, EE_EINVAL, "bad tensor name " + name);
+    const int l = atoi(name.substr(7, dot - 7).c_str());
+    const std::string leaf = name.substr(dot + 1);
+    if (l < 0 || l >= g.n_layers || name.substr(7, dot - 7) != std::to_string(l))
+      return fail(c, EE_EINVAL, "bad layer index in " + name);
+    const size_t rb = static_cast<size_t>(H * es);
+    char* qkv = static_cast<char*>(c->wqkv[l]);
+    const char* src = static_cast<const char*>(t.ptr);
+    if (leaf == "attn_norm" || leaf == "mlp_norm") {
+      if ((r = need(H * 4))) return r;
+      HIPCHK(c, hipMemcpy(leaf == "attn_norm" ? c->g_attn[l] : c->g_mlp[l], t.ptr, t.nbytes,
+                          hipMemcpyDefault));
+    } else if (leaf == "wq") {
+      if ((r = need(A * D * H * es))) return r;
+      if ((r = copy_rope_heads(c, qkv, src, static_cast<int>(A)))) return r;
+    } else if (leaf == "wk") {
+      if ((r = need(K * D * H * es))) return r;
+      if ((r = copy_rope_heads(c, qkv + A * D * rb, src, static_cast<int>(K)))) return r;
+    } else if (leaf == "wv") {
+      if ((r = need(K * D * H * es))) return r;
+      HIPCHK(c, hipMemcpy(qkv + (A + K) * D * rb, t.ptr, t.nbytes, hipMemcpyDefault));
+    } else if (leaf == "wo") {
+      if ((r = need(H * A * D * es))) return r;
+      HIPCHK(c, hipMemcpy(c->wo[l], t.ptr, t.nbytes, hipMemcpyDefault));
+    } else if (leaf == "w_gate" || leaf == "w_up") {
+      if ((r = need(F * H * es))) return r;
+      char* dst = static_cast<char*>(c->wgu[l]) + (leaf == "w_up" ? rb : 0);
+      if ((r = copy_rows(c, dst, 2 * rb, src, rb, rb, static_cast<size_t>(F)))) return r;
+    } else if (leaf == "w_down") {
+      if ((r = need(H * F * es))) return r;
+      HIPCHK(c, hipMemcpy(c->wd[l], t.ptr, t.nbytes, hipMemcpyDefault));
+    } else {
+      return fail(c, EE_EINVAL, "unknown tensor " + name);
+    }
+  } else if (name.rfind("readout.", 0) == 0) {
+    const size_t dot = name.find('.', 8);
+    if (dot == std::string::npos) return fail(c, EE_EINVAL, "bad tensor name " + name);
+    const int L = atoi(name.substr(8, dot - 8).c_str());
+    const std::string leaf = name.substr(dot + 1);
+    if (L < 1 || L > g.n_layers || name.substr(8, dot - 8) != std::to_string(L))
+      return fail(c, EE_EINVAL, "readout layer must be 1..n_layers in " + name);
+    if (leaf != "w" && leaf != "b") return fail(c, EE_EINVAL, "unknown tensor " + name);
+    if ((r = need(leaf == "w" ? H * H * es : H * 4))) return r;
+    if (!c->readout.count(L)) {
+      void* w = nullptr;
+      float* b = nullptr;
+      if ((r = dalloc(c, &w, static_cast<size_t>(H * H * es)))) return r;
+      if ((r = dalloc(c, &b, static_cast<size_t>(H * 4)))) {
+        dfree(w);
+        return r;
+      }
+      c->readout[L] = {w, b};
+    }
+    auto& ro = c->readout[L];
+    HIPCHK(c, hipMemcpy(leaf == "w" ? ro.first : static_cast<void*>(ro.second), t.ptr, t.nbytes,
+                        hipMemcpyDefault));
+    return EE_OK;  // readouts are not part of the required set
+  } else {
+    return fail(c, EE_EINVAL, "unknown tensor " + name);
+  }
+  c->loaded.insert(name);
+  return EE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ee_create(const ee_config* cfg, void* hip_stream, ee_ctx** out) {
+  if (!cfg || !out) return EE_EINVAL;
+  *out = nullptr;
+  std::string why;
+  g_create_err.clear();
+  if (!validate_config(cfg, why)) {
+    g_create_err = why;
+    return EE_EINVAL;
+  }
+  ee_ctx* c = new (std::nothrow) ee_ctx();
+  if (!c) {
+    g_create_err = "out of host memory";
+    return EE_ENOMEM;
+  }
+  c->cfg = *cfg;
+  c->wbf16 = cfg->wdtype == EE_BF16;
+  c->esz = c->wbf16 ? 2 : 4;
+  int r = EE_OK;
+  auto bail = [&](int code) {
+    g_create_err = c->err.empty() ? "ee_create failed" : c->err;
+    ee_destroy(c);
+    return code;
+  };
+  hipError_t he;
+  if ((he = hipGetDevice(&c->device)) != hipSuccess) return bail(hip_fail(c, he, "hipGetDevice"));
+  if ((he = hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, c->device)) != hipSuccess)
+    return bail(hip_fail(c, he, "hipDeviceGetAttribute"));
+  if (hip_stream) {
+    c->stream = static_cast<hipStream_t>(hip_stream);
+  } else {
+    if ((he = hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking)) != hipSuccess)
+      return bail(hip_fail(c, he, "hipStreamCreateWithFlags"));
+    c->own_stream = true;
+  }
+  if ((he = hipEventCreate(&c->ev0)) != hipSuccess || (he = hipEventCreate(&c->ev1)) != hipSuccess)
+    return bail(hip_fail(c, he, "hipEventCreate"));
+  const ee_config& g = *cfg;
+  const size_t es = c->esz;
+  const size_t H = g.hidden, A = g.n_q_heads, K = g.n_kv_heads, D = g.head_dim, F = g.ffn,
+               V = g.vocab, L = g.n_layers;
+  if ((r = dalloc(c, &c->embed, V * H * es))) return bail(r);
+  c->wqkv.assign(L, nullptr); c->wo.assign(L, nullptr); c->wgu.assign(L, nullptr);
+  c->wd.assign(L, nullptr); c->g_attn.assign(L, nullptr); c->g_mlp.assign(L, nullptr);
+  for (size_t l = 0; l < L; ++l) {
+    if ((r = dalloc(c, &c->wqkv[l], (A + 2 * K) * D * H * es))) return bail(r);
+    if ((r = dalloc(c, &c->wo[l], H * A * D * es))) return bail(r);
+    if ((r = dalloc(c, &c->wgu[l], 2 * F * H * es))) return bail(r);
+    if ((r = dalloc(c, &c->wd[l], H * F * es))) return bail(r);
+    if ((r = dalloc(c, &c->g_attn[l], H * 4))) return bail(r);
+    if ((r = dalloc(c, &c->g_mlp[l], H * 4))) return bail(r);
+  }
+  if ((r = dalloc(c, &c->g_final, H * 4))) return bail(r);
+  if ((r = dalloc(c, &c->d_layers, L * sizeof(ee::LayerW)))) return bail(r);
+  {
+    std::vector<ee::LayerW> lw(L);
+    for (size_t l = 0; l < L; ++l)
+      lw[l] = ee::LayerW{c->wqkv[l], c->wo[l], c->wgu[l], c->wd[l], c->g_attn[l], c->g_mlp[l]};
+    if ((he = hipMemcpy(c->d_layers, lw.data(), L * sizeof(ee::LayerW), hipMemcpyHostToDevice)) != hipSuccess)
+      return bail(hip_fail(c, he, "hipMemcpy layer table"));
+  }
+  c->n_pages = (g.max_seq + g.page_size - 1) / g.page_size;
+  c->layer_stride = static_cast<int64_t>(c->n_pages) * K * g.page_size * D;
+  if ((r = dalloc(c, &c->kpool, L * c->layer_stride * es))) return bail(r);
+  if ((r = dalloc(c, &c->vpool, L * c->layer_stride * es))) return bail(r);
+  if ((r = dalloc(c, &c->d_block_table, sizeof(int32_t) * c->n_pages))) return bail(r);
+  if ((he = hipHostMalloc(reinterpret_cast<void**>(&c->h_block_table), sizeof(int32_t) * c->n_pages)) != hipSuccess)
+    return bail(hip_fail(c, he, "hipHostMalloc block table"));
+  reset_pages(c);
+  // RoPE: angle = pos * base^(-2i/D), computed in double, stored as float.
+  {
+    const size_t half = D / 2;
+    std::vector<float> cs(static_cast<size_t>(g.max_seq) * half), sn(cs.size());
+    for (int t = 0; t < g.max_seq; ++t)
+      for (size_t i = 0; i < half; ++i) {
+        const double inv = pow(static_cast<double>(g.rope_base), -2.0 * static_cast<double>(i) / D);
+        const double ang = static_cast<double>(t) * inv;
+        cs[t * half + i] = static_cast<float>(cos(ang));
+        sn[t * half + i] = static_cast<float>(sin(ang));
+      }
+    if ((r = dalloc(c, &c->d_cos, cs.size() * 4))) return bail(r);
+    if ((r = dalloc(c, &c->d_sin, sn.size() * 4))) return bail(r);
+    if ((he = hipMemcpy(c->d_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice)) != hipSuccess ||
+        (he = hipMemcpy(c->d_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
+      return bail(hip_fail(c, he, "hipMemcpy rope tables"));
+  }
+  if ((r = dalloc(c, &c->d_h, H * 4)) || (r = dalloc(c, &c->d_hexit, H * 4)) ||
+      (r = dalloc(c, &c->d_z, H * 4)) || (r = dalloc(c, &c->d_q, A * D * 4)) ||
+      (r = dalloc(c, &c->d_o, A * D * 4)) || (r = dalloc(c, &c->d_a, F * 4)) ||
+      (r = dalloc(c, &c->d_x, H * 4)))
+    return bail(r);
+  c->max_splits = (g.max_seq + ee::kAttnSplit - 1) / ee::kAttnSplit;
+  if ((r = dalloc(c, &c->d_attn_part, K * c->max_splits * (A / K) * (D + 2) * 4))) return bail(r);
+  if ((r = dalloc(c, &c->d_counters, sizeof(ee::Counters)))) return bail(r);
+  if ((r = dalloc(c, &c->d_ctl, sizeof(ee::StepCtl)))) return bail(r);
+
+  DevParams p = make_params(c, INFINITY, 0);
+  c->lds = ee::lds_bytes(p);
+  const int per_cu = ee::persistent_max_wgs_per_cu(c->wbf16, c->lds);
+  c->nwg_persistent = per_cu > 0 ? c->n_cu * std::min(per_cu, 2) : 0;
+  c->head_wgs = 4 * c->n_cu;
+  c->max_parts = std::max(c->head_wgs, c->nwg_persistent);
+  if ((r = dalloc(c, &c->d_head_part, static_cast<size_t>(c->max_parts) * 4 * 4))) return bail(r);
+  *out = c;
+  return EE_OK;
+}
+
+int ee_load_weights(ee_ctx* c, const ee_tensor* tensors, int32_t n_tensors) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  if (!tensors || n_tensors < 0) return fail(c, EE_EINVAL, "bad tensor list");
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  for (int i = 0; i < n_tensors; ++i) {
+    const int r = load_one(c, tensors[i]);
+    if (r) return r;
+  }
+  HIPCHK(c, hipDeviceSynchronize());
+  return EE_OK;
+}
+
+int ee_prefill(ee_ctx* c, const int32_t* tokens, int32_t n, int32_t* out_first_token) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  if (!weights_ready(c)) return fail(c, EE_ESTATE, "weights not fully loaded");
+  if (!tokens || n <= 0) return fail(c, EE_EINVAL, "prefill needs at least one token");
+  int r;
+  if ((r = upload_force(c, n, tokens, nullptr))) return r;
+  if ((r = run_steps(c, INFINITY, 0, n, c->d_force_tok, nullptr, true, false))) return r;
+  int32_t tok = -1;
+  HIPCHK(c, hipMemcpy(&tok, c->d_ring_tok + (n - 1), sizeof(tok), hipMemcpyDeviceToHost));
+  if (out_first_token) *out_first_token = tok;
+  return EE_OK;
+}
+
+int ee_decode_n_ex(ee_ctx* c, float tau, int32_t exit_layer, int32_t n, const int32_t* force_tokens,
+                   const int32_t* force_exit, int32_t* tokens, int32_t* exited, float* conf,
+                   int32_t* would_exit) {
+  int r = decode_common(c, tau, exit_layer, n, force_tokens, force_exit, false);
+  if (r) return r;
+  return copy_ring(c, n, tokens, exited, conf, would_exit);
+}
+
+int ee_decode_n(ee_ctx* c, float tau, int32_t exit_layer, int32_t n, int32_t* tokens,
+                int32_t* exited, float* conf) {
+  return ee_decode_n_ex(c, tau, exit_layer, n, nullptr, nullptr, tokens, exited, conf, nullptr);
+}
+
+int ee_decode_step(ee_ctx* c, float tau, int32_t exit_layer, int32_t* out_token,
+                   int32_t* out_exited, float* out_conf) {
+  return ee_decode_n_ex(c, tau, exit_layer, 1, nullptr, nullptr, out_token, out_exited, out_conf,
+                        nullptr);
+}
+
+int ee_decode_step_ex(ee_ctx* c, float tau, int32_t exit_layer, int32_t input_token,
+                      int32_t force_exit, ee_debug* dbg) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  int r;
+  const bool want_logits = dbg && (dbg->logits_readout || dbg->logits_full);
+  if (want_logits && !c->d_dbg_r) {
+    if ((r = dalloc(c, &c->d_dbg_r, static_cast<size_t>(c->cfg.vocab) * 4))) return r;
+    if ((r = dalloc(c, &c->d_dbg_f, static_cast<size_t>(c->cfg.vocab) * 4))) return r;
+  }
+  const int32_t ft[1] = {input_token};
+  const int32_t fe[1] = {force_exit};
+  r = decode_common(c, tau, exit_layer, 1, input_token >= 0 ? ft : nullptr,
+                    force_exit >= 0 ? fe : nullptr, want_logits);
+  if (r) return r;
+  if (!dbg) return EE_OK;
+  ee::StepCtl ctl;
+  HIPCHK(c, hipMemcpy(&ctl, c->d_ctl, sizeof(ctl), hipMemcpyDeviceToHost));
+  int32_t tok = 0, ex = 0, would = 0;
+  float cf = 0.f;
+  if ((r = copy_ring(c, 1, &tok, &ex, &cf, &would))) return r;
+  const size_t H = c->cfg.hidden, V = c->cfg.vocab;
+  dbg->token = tok;
+  dbg->exited = ex;
+  dbg->would_exit = would;
+  dbg->conf = cf;
+  dbg->readout_token = exit_layer > 0 ? ctl.readout_token : -1;
+  dbg->full_token = ex ? -1 : ctl.full_token;
+  dbg->conf_full = ex ? NAN : ctl.conf_full;
+  if (dbg->h_exit && exit_layer > 0)
+    HIPCHK(c, hipMemcpy(dbg->h_exit, c->d_hexit, H * 4, hipMemcpyDeviceToHost));
+  if (dbg->h_final && !ex) HIPCHK(c, hipMemcpy(dbg->h_final, c->d_h, H * 4, hipMemcpyDeviceToHost));
+  if (dbg->logits_readout && exit_layer > 0)
+    HIPCHK(c, hipMemcpy(dbg->logits_readout, c->d_dbg_r, V * 4, hipMemcpyDeviceToHost));
+  if (dbg->logits_full && !ex)
+    HIPCHK(c, hipMemcpy(dbg->logits_full, c->d_dbg_f, V * 4, hipMemcpyDeviceToHost));
+  return EE_OK;
+}
+
+int ee_calibrate_threshold(ee_ctx* c, const int32_t* prompts, const int32_t* prompt_lens,
+                           int32_t n_prompts, int32_t n_gen, int32_t exit_layer, int32_t mode,
+                           float target, float* out_tau) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  if (!prompts || !prompt_lens || n_prompts <= 0 || n_gen <= 0 || !out_tau)
+    return fail(c, EE_EINVAL, "calibration needs prompts, n_gen > 0 and an output");
+  if (exit_layer < 1) return fail(c, EE_EINVAL, "calibration needs a gated exit layer");
+  if (mode != EE_CAL_EXIT_RATE && mode != EE_CAL_MEDIAN) return fail(c, EE_EINVAL, "unknown mode");
+  if (mode == EE_CAL_EXIT_RATE && !(target >= 0.f && target <= 1.f))
+    return fail(c, EE_EINVAL, "target exit rate must be in [0, 1]");
+  int r;
+  if ((r = check_gate_args(c, INFINITY, exit_layer))) return r;
+  std::vector<float> confs;
+  std::vector<float> buf(n_gen);
+  size_t off = 0;
+  for (int i = 0; i < n_prompts; ++i) {
+    if (prompt_lens[i] <= 0) return fail(c, EE_EINVAL, "empty calibration prompt");
+    if ((r = ee_reset(c))) return r;
+    int32_t first = 0;
+    if ((r = ee_prefill(c, prompts + off, prompt_lens[i], &first))) return r;
+    if ((r = ee_decode_n(c, INFINITY, exit_layer, n_gen, nullptr, nullptr, buf.data()))) return r;
+    confs.insert(confs.end(), buf.begin(), buf.end());
+    off += prompt_lens[i];
+  }
+  if ((r = ee_reset(c))) return r;
+  std::sort(confs.begin(), confs.end());
+  const size_t n = confs.size();
+  if (mode == EE_CAL_MEDIAN) {
+    const double med = n % 2 ? confs[n / 2]
+                             : 0.5 * (static_cast<double>(confs[n / 2 - 1]) + confs[n / 2]);
+    *out_tau = static_cast<float>(med);
+  } else {
+    const size_t k = static_cast<size_t>(floor(static_cast<double>(target) * n + 0.5));
+    if (k == 0) *out_tau = INFINITY;
+    else if (k >= n) *out_tau = -INFINITY;
+    else *out_tau = confs[n - k - 1];
+  }
+  return EE_OK;
+}
+
+int ee_set_readout_bias(ee_ctx* c, int32_t exit_layer, const float* b, int32_t on_device) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  auto it = c->readout.find(exit_layer);
+  if (it == c->readout.end() || !b) return fail(c, EE_EINVAL, "no readout at that layer");
+  HIPCHK(c, hipMemcpyAsync(it->second.second, b, sizeof(float) * c->cfg.hidden,
+                           on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice, c->stream));
+  return EE_OK;
+}
+
+int ee_head_eval(ee_ctx* c, int32_t readout_layer, const float* x, int32_t* out_token,
+                 float* out_conf, float* out_logits) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  if (!x) return fail(c, EE_EINVAL, "x is null");
+  int r;
+  if ((r = check_gate_args(c, INFINITY, readout_layer))) return r;
+  if (out_logits && !c->d_dbg_r) {
+    if ((r = dalloc(c, &c->d_dbg_r, static_cast<size_t>(c->cfg.vocab) * 4))) return r;
+    if ((r = dalloc(c, &c->d_dbg_f, static_cast<size_t>(c->cfg.vocab) * 4))) return r;
+  }
+  HIPCHK(c, hipMemcpyAsync(c->d_x, x, sizeof(float) * c->cfg.hidden, hipMemcpyHostToDevice, c->stream));
+  DevParams p = make_params(c, INFINITY, readout_layer);
+  if (out_logits) {
+    p.dbg_logits_r = c->d_dbg_r;
+    p.dbg_logits_f = c->d_dbg_f;
+  }
+  ee::StepCtl saved;
+  HIPCHK(c, hipMemcpy(&saved, c->d_ctl, sizeof(saved), hipMemcpyDeviceToHost));
+  HIPCHK(c, hipMemsetAsync(reinterpret_cast<char*>(c->d_ctl) + offsetof(ee::StepCtl, exited), 0,
+                           offsetof(ee::StepCtl, pad) - offsetof(ee::StepCtl, exited), c->stream));
+  hipError_t e = ee::launch_head_eval(p, c->wbf16, c->d_x, readout_layer > 0, c->head_wgs, c->stream);
+  if (e != hipSuccess) return hip_fail(c, e, "head eval launch");
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  ee::StepCtl ctl;
+  HIPCHK(c, hipMemcpy(&ctl, c->d_ctl, sizeof(ctl), hipMemcpyDeviceToHost));
+  // the eval's head wrote next_token: restore the sequence's
+  HIPCHK(c, hipMemcpy(&c->d_ctl->next_token, &saved.next_token, sizeof(int32_t), hipMemcpyHostToDevice));
+  if (out_token) *out_token = readout_layer > 0 ? ctl.readout_token : ctl.full_token;
+  if (out_conf) *out_conf = readout_layer > 0 ? ctl.conf : ctl.conf_full;
+  if (out_logits)
+    HIPCHK(c, hipMemcpy(out_logits, readout_layer > 0 ? c->d_dbg_r : c->d_dbg_f,
+                        sizeof(float) * c->cfg.vocab, hipMemcpyDeviceToHost));
+  return EE_OK;
+}
+
+int ee_read_kv(ee_ctx* c, int32_t layer, int32_t pos, float* k_out, float* v_out) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  if (layer < 0 || layer >= c->cfg.n_layers || pos < 0 || pos >= c->pos)
+    return fail(c, EE_EINVAL, "layer or position out of range");
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  const int K = c->cfg.n_kv_heads, D = c->cfg.head_dim, P = c->cfg.page_size;
+  const int page = c->h_block_table[pos / P], slot = pos % P;
+  std::vector<unsigned char> buf(static_cast<size_t>(D) * c->esz);
+  for (int pass = 0; pass < 2; ++pass) {
+    float* out = pass ? v_out : k_out;
+    if (!out) continue;
+    const char* pool = static_cast<const char*>(pass ? c->vpool : c->kpool);
+    for (int h = 0; h < K; ++h) {
+      const int64_t off = static_cast<int64_t>(layer) * c->layer_stride +
+                          ((static_cast<int64_t>(page) * K + h) * P + slot) * D;
+      HIPCHK(c, hipMemcpy(buf.data(), pool + off * c->esz, buf.size(), hipMemcpyDeviceToHost));
+      for (int d = 0; d < D; ++d) {
+        float f;
+        if (c->wbf16) {
+          uint16_t b;
+          memcpy(&b, buf.data() + 2 * d, 2);
+          const uint32_t u = static_cast<uint32_t>(b) << 16;
+          memcpy(&f, &u, 4);
+        } else {
+          memcpy(&f, buf.data() + 4 * d, 4);
+        }
+        // keys are stored with rotate-half pairs interleaved: element 2i is
+        // dimension i, element 2i+1 is dimension i + D/2
+        const int dim = pass ? d : ((d & 1) ? D / 2 + d / 2 : d / 2);
+        out[h * D + dim] = f;
+      }
+    }
+  }
+  return EE_OK;
+}
+
+int ee_set_persistent(ee_ctx* c, int32_t on) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  if (on && c->nwg_persistent <= 0)
+    return fail(c, EE_ESTATE, "persistent kernel cannot be co-resident on this device");
+  c->persistent = on != 0;
+  return EE_OK;
+}
+
+int ee_last_decode_ms(ee_ctx* c, float* out_ms) {
+  if (!c || !out_ms) return EE_EINVAL;
+  *out_ms = c->last_ms;
+  return EE_OK;
+}
+
+int32_t ee_position(const ee_ctx* c) { return c ? c->pos : -1; }
+
+int ee_reset(ee_ctx* c) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  c->pos = 0;
+  c->have_next = false;
+  reset_pages(c);
+  HIPCHK(c, hipMemset(c->d_ctl, 0, sizeof(ee::StepCtl)));
+  HIPCHK(c, hipMemset(c->d_counters, 0, sizeof(ee::Counters)));
+  HIPCHK(c, hipDeviceSynchronize());
+  return EE_OK;
+}
+
+const char* ee_last_error(const ee_ctx* c) { return c ? c->err.c_str() : g_create_err.c_str(); }
+
+void ee_destroy(ee_ctx* c) {
+  if (!c) return;
+  if (c->stream) (void)hipStreamSynchronize(c->stream);
+  dfree(c->embed);
+  for (void* p : c->wqkv) dfree(p);
+  for (void* p : c->wo) dfree(p);
+  for (void* p : c->wgu) dfree(p);
+  for (void* p : c->wd) dfree(p);
+  for (float* p : c->g_attn) dfree(p);
+  for (float* p : c->g_mlp) dfree(p);
+  dfree(c->g_final);
+  for (auto& kv : c->readout) {
+    dfree(kv.second.first);
+    dfree(kv.second.second);
+  }
+  dfree(c->d_layers); dfree(c->kpool); dfree(c->vpool); dfree(c->d_block_table);
+  if (c->h_block_table) (void)hipHostFree(c->h_block_table);
+  dfree(c->d_cos); dfree(c->d_sin);
+  dfree(c->d_h); dfree(c->d_hexit); dfree(c->d_z); dfree(c->d_q); dfree(c->d_o); dfree(c->d_a);
+  dfree(c->d_x); dfree(c->d_attn_part); dfree(c->d_head_part); dfree(c->d_counters); dfree(c->d_ctl);
+  dfree(c->d_ring_tok); dfree(c->d_ring_exit); dfree(c->d_ring_would); dfree(c->d_ring_conf);
+  dfree(c->d_force_tok); dfree(c->d_force_exit); dfree(c->d_dbg_r); dfree(c->d_dbg_f);
+  if (c->ev0) (void)hipEventDestroy(c->ev0);
+  if (c->ev1) (void)hipEventDestroy(c->ev1);
+  if (c->own_stream && c->stream) (void)hipStreamDestroy(c->stream);
+  delete c;
+}
+
+}  // extern "C"

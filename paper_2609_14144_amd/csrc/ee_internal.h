@@ -1,0 +1,118 @@
+// Internal types shared by the runtime (ee_api.hip) and the kernels
+// (ee_kernels.hip). Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ee {
+
+constexpr int kWG = 256;               // threads per workgroup, every kernel
+constexpr int kWaves = kWG / 64;       // 64-wide wavefronts per workgroup
+constexpr int kAttnSplit = 64;         // positions per attention work item
+constexpr int kMaxGroup = 8;           // max query heads per KV head
+constexpr int kMaxHeadDim = 256;
+
+// Per-layer device pointers, repacked layouts:
+//   wqkv [(A + 2K) * D][H]: q rows, then k rows, then v rows. Within every q
+//        and k head the rows are pair-interleaved: row 2i is the original row
+//        i and row 2i+1 the original row i + D/2, so one wave computes both
+//        halves of a rotate-half RoPE pair.
+//   wo   [H][A*D]
+//   wgu  [2F][H]: row 2j = gate row j, row 2j+1 = up row j.
+//   wd   [H][F]
+struct LayerW {
+  const void* wqkv;
+  const void* wo;
+  const void* wgu;
+  const void* wd;
+  const float* g_attn;
+  const float* g_mlp;
+};
+
+// Device-side control record of the step being run (one per context).
+struct StepCtl {
+  int32_t next_token;     // input of the next step (last emitted token)
+  int32_t exited;         // branch taken by the current step
+  int32_t would_exit;     // gate decision before forcing
+  int32_t readout_token;
+  int32_t full_token;
+  float conf;             // readout confidence
+  float conf_full;        // full head confidence
+  int32_t error;          // nonzero: device-side failure (see kErr*)
+  uint32_t abort;         // set when a bounded wait times out; everything drains
+  uint32_t pad[7];
+};
+
+enum : int32_t { kErrNone = 0, kErrBarrier = 1, kErrToken = 2 };
+
+// Grid barrier / last-arriver counters. Each lives on its own 256-byte line.
+struct Counters {
+  uint32_t barrier[64];
+  uint32_t attn[64 * 16];   // per KV head (index kvh * 64)
+  uint32_t head[64];
+};
+
+struct DevParams {
+  // shapes
+  int L, H, A, K, D, F, V, G;   // G = A / K
+  int qkv_rows;                 // (A + 2K) * D
+  float eps;
+  float attn_scale;             // 1/sqrt(D)
+  float tau;
+  int exit_layer;               // 0 = ungated
+  int page_size, page_shift;
+  // weights
+  const void* embed;            // [V][H]
+  const LayerW* layers;         // [L] (device array)
+  const float* g_final;         // [H]
+  const void* ro_w;             // readout at exit_layer [H][H] (null if ungated)
+  const float* ro_b;            // [H]
+  // KV cache: pool[layer][page][kv_head][slot][D]
+  void* kpool;
+  void* vpool;
+  int64_t layer_stride;         // elements per layer
+  const int32_t* block_table;   // logical page -> physical page
+  const float* rope_cos;        // [max_seq][D/2]
+  const float* rope_sin;
+  // activations (fp32)
+  float* h;                     // [H] residual stream
+  float* h_exit;                // [H]
+  float* z;                     // [H] readout output
+  float* q;                     // [A*D]
+  float* o;                     // [A*D]
+  float* a;                     // [F]
+  float* attn_part;             // [K][max_splits][G][D + 2]
+  int max_splits;
+  float* head_part;             // [max_parts][4]
+  int max_parts;
+  Counters* counters;
+  StepCtl* ctl;
+  // per-call ring (device arrays of n)
+  int32_t* ring_tok;
+  int32_t* ring_exit;
+  int32_t* ring_would;
+  float* ring_conf;
+  const int32_t* force_tok;     // may be null
+  const int32_t* force_exit;    // may be null
+  // debug outputs (device, may be null; only meaningful for single steps)
+  float* dbg_logits_r;
+  float* dbg_logits_f;
+  float* dbg_h_final;
+};
+
+// Host launchers (defined in ee_kernels.hip).
+hipError_t launch_decode_per_op(const DevParams& p, int wbf16, int pos0, int n, int head_wgs,
+                                hipStream_t s);
+hipError_t launch_decode_persistent(const DevParams& p, int wbf16, int pos0, int n, int nwg,
+                                    size_t lds, hipStream_t s);
+hipError_t launch_prefill_per_op(const DevParams& p, int wbf16, int pos0, const int32_t* d_tokens,
+                                 int n, int head_wgs, hipStream_t s);
+hipError_t launch_prefill_persistent(const DevParams& p, int wbf16, int pos0, int n, int nwg,
+                                     size_t lds, hipStream_t s);
+hipError_t launch_head_eval(const DevParams& p, int wbf16, const float* d_x, int readout,
+                            int head_wgs, hipStream_t s);
+size_t lds_bytes(const DevParams& p);
+int persistent_max_wgs_per_cu(int wbf16, size_t lds);
+
+}  // namespace ee

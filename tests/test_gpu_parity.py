@@ -1,0 +1,384 @@
+"""GPU parity: the HIP decode path (through the C ABI) against the CPU oracle
+on identical seeded inputs. See tests/gpu_helpers.py for the comparison rule."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.conftest import weights_for
+from tests.gpu_helpers import (MARGIN, compare_step, engine, lockstep, oracle_for, rel)
+
+pytestmark = pytest.mark.gpu
+
+TINY_P = 16
+TINY_N = 32
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+_TAU = {}
+
+
+def tiny_tau(name):
+    """Median readout confidence of an oracle calibration run: 8 seeded
+    prompts (seeds 100..107) of 16 tokens, 32 full-depth steps each."""
+    if name not in _TAU:
+        cfg = synth.get_config(name)
+        confs = []
+        for seed in range(100, 108):
+            o = oracle_for(name, TINY_P + TINY_N)
+            g = o.prefill(synth.prompts(cfg, seed, TINY_P))
+            confs += [r.conf for r in o.generate(g, math.inf, 2, TINY_N)]
+        _TAU[name] = oracle.tau_median(confs)
+    return _TAU[name]
+
+
+@pytest.mark.parametrize("persistent", [True, False], ids=["persistent", "per_op"])
+@pytest.mark.parametrize("name", ["tiny", "tiny_bf16"])
+def test_tiny_lockstep(name, persistent):
+    cfg = synth.get_config(name)
+    tau = tiny_tau(name)
+    prompt = synth.prompts(cfg, 1, TINY_P)
+    o = oracle_for(name, 128)
+    e = engine(name, 128, persistent)
+    g0 = o.prefill(prompt)
+    g0_gpu = e.ee_prefill(prompt)
+    if o.last_prefill_stats[2] > MARGIN:
+        assert g0_gpu == g0
+    rep, outside = lockstep(e, o, g0, tau, 2, TINY_N)
+    # teacher-forced continuation with varied inputs
+    toks = synth.prompts(cfg, 5, TINY_N)
+    rep2, outside2 = lockstep(e, o, None, tau, 2, TINY_N, force_tokens=toks)
+    assert outside + outside2 >= 2 * TINY_N - 4
+    worst = max(r for _, r in rep + rep2)
+    print(f"{name} persistent={persistent} tau={tau:.4f} worst rel err {worst:.2e}")
+
+
+@pytest.mark.parametrize("name", ["tiny", "tiny_bf16"])
+def test_tiny_both_branches_exercised(name):
+    cfg = synth.get_config(name)
+    tau = tiny_tau(name)
+    o = oracle_for(name, 128)
+    g0 = o.prefill(synth.prompts(cfg, 1, TINY_P))
+    rs = o.generate(g0, tau, 2, TINY_N, force_tokens=synth.prompts(cfg, 5, TINY_N))
+    n_exit = sum(r.exited for r in rs)
+    assert 0 < n_exit < TINY_N
+
+
+@pytest.mark.parametrize("persistent", [True, False], ids=["persistent", "per_op"])
+def test_tiny_decode_n_imposed_and_gated(persistent):
+    """n steps in one call (the timed entry point) with teacher-forced inputs;
+    first with the gate's own decisions, then with imposed exits."""
+    name = "tiny_bf16"
+    cfg = synth.get_config(name)
+    tau = tiny_tau(name)
+    prompt = synth.prompts(cfg, 1, TINY_P)
+    toks = synth.prompts(cfg, 6, TINY_N)
+    for fe in (None, (np.arange(TINY_N) % 3 == 0).astype(np.int32)):
+        o = oracle_for(name, 128)
+        o.prefill(prompt)
+        rs = o.generate(None, tau, 2, TINY_N, force_tokens=toks, force_exit=fe)
+        e = engine(name, 128, persistent)
+        e.ee_prefill(prompt)
+        tok, ex, conf, would = e.ee_decode_n_ex(tau, 2, TINY_N, force_tokens=toks, force_exit=fe)
+        for i, r in enumerate(rs):
+            assert abs(conf[i] - r.conf) <= 1e-4 + 1e-3 * r.conf
+            if abs(r.conf - tau) > MARGIN:
+                assert would[i] == r.would_exit
+                if fe is None:
+                    assert ex[i] == r.exited
+            if fe is not None:
+                assert ex[i] == bool(fe[i])
+            gap = r.gap_readout if r.exited else r.gap_full
+            if gap > MARGIN and ex[i] == r.exited:
+                assert tok[i] == r.token, i
+        assert e.ee_position() == TINY_P + TINY_N
+
+
+def test_tiny_free_running_matches_until_first_margin():
+    name = "tiny_bf16"
+    cfg = synth.get_config(name)
+    tau = tiny_tau(name)
+    for seed in (1, 2, 3):
+        prompt = synth.prompts(cfg, seed, TINY_P)
+        o = oracle_for(name, 128)
+        g0 = o.prefill(prompt)
+        rs = o.generate(g0, tau, 2, TINY_N)
+        e = engine(name, 128)
+        assert e.ee_prefill(prompt) == g0
+        tok, ex, conf = e.ee_decode_n(tau, 2, TINY_N)
+        for i, r in enumerate(rs):
+            gap = r.gap_readout if r.exited else r.gap_full
+            if abs(r.conf - tau) <= MARGIN or gap <= MARGIN:
+                break
+            assert ex[i] == r.exited and tok[i] == r.token, (seed, i)
+            assert abs(conf[i] - r.conf) <= 1e-4 + 1e-3 * r.conf
+
+
+@pytest.mark.parametrize("name", ["tiny", "tiny_bf16"])
+def test_kv_cache_contents_including_fill(name):
+    cfg = synth.get_config(name)
+    prompt = synth.prompts(cfg, 1, TINY_P)
+    toks = synth.prompts(cfg, 7, 8)
+    fe = np.array([1, 0, 1, 1, 0, 1, 0, 1], np.int32)
+    o = oracle_for(name, 64)
+    o.prefill(prompt)
+    o.generate(None, 0.5, 2, 8, force_tokens=toks, force_exit=fe)
+    e = engine(name, 64, page_size=16)
+    e.ee_prefill(prompt)
+    e.ee_decode_n_ex(0.5, 2, 8, force_tokens=toks, force_exit=fe)
+    bad = 0
+    total = 0
+    for l in range(cfg.n_layers):
+        for t in range(TINY_P + 8):
+            k, v = e.ee_read_kv(l, t)
+            for got, ref in ((k, o.kcache[l, t].reshape(-1)), (v, o.vcache[l, t].reshape(-1))):
+                err = np.abs(got - ref)
+                # fp32 accumulation over H terms: a few ulps of the vector's scale
+                tol = np.full(err.shape, 1e-5 * np.max(np.abs(ref)))
+                if cfg.wdtype == "bf16":
+                    # identical storage rounding: equal, or one bf16 step apart where
+                    # the fp32 value sat within accumulation noise of a midpoint
+                    tol = np.maximum(tol, np.abs(ref) * 2.0 ** -7 * 1.01)
+                    bad += int(np.sum(err > 0))
+                assert np.all(err <= tol + 1e-30), (l, t, float(err.max()))
+                total += got.size
+    assert bad <= max(4, total // 200), (bad, total)
+
+
+def test_error_paths():
+    from paper_2609_14144_amd import EEError
+    name = "tiny"
+    cfg = synth.get_config(name)
+    e = engine(name, 24)
+    with pytest.raises(EEError) as ei:
+        e.ee_decode_step(0.5, 2)
+    assert ei.value.code == -2  # decode before prefill
+    e.ee_prefill(synth.prompts(cfg, 1, 16))
+    with pytest.raises(EEError) as ei:
+        e.ee_decode_step(0.5, 3)  # no readout at layer 3
+    assert ei.value.code == -1
+    with pytest.raises(EEError) as ei:
+        e.ee_decode_step(float("nan"), 2)
+    assert ei.value.code == -1
+    with pytest.raises(EEError) as ei:
+        e.ee_decode_step(0.5, 9)
+    assert ei.value.code == -1
+    with pytest.raises(EEError) as ei:
+        e.ee_decode_n_ex(0.5, 2, 2, force_tokens=[0, cfg.vocab])
+    assert ei.value.code == -1
+    e.ee_decode_n(0.5, 2, 8)                  # fills to capacity 24
+    with pytest.raises(EEError) as ei:
+        e.ee_decode_step(0.5, 2)
+    assert ei.value.code == -5
+    with pytest.raises(EEError) as ei:
+        e.ee_load_weights({"embed": np.zeros(3, np.float32)})
+    assert ei.value.code == -1
+    with pytest.raises(EEError) as ei:
+        e.ee_load_weights({"layers.0.bogus": np.zeros(3, np.float32)})
+    assert ei.value.code == -1
+    e.ee_reset()
+    assert e.ee_position() == 0
+    assert e.ee_prefill(synth.prompts(cfg, 1, 16)) >= 0   # usable after errors
+    from paper_2609_14144_amd import Engine
+    e2 = Engine(cfg, 32)
+    with pytest.raises(EEError) as ei:
+        e2.ee_prefill([1, 2, 3])
+    assert ei.value.code == -2  # weights not loaded
+
+
+def test_gate_limits_and_ungated_equivalence():
+    name = "tiny_bf16"
+    cfg = synth.get_config(name)
+    prompt = synth.prompts(cfg, 1, TINY_P)
+    toks = synth.prompts(cfg, 5, 16)
+    out = {}
+    for key, tau, Le in (("inf", math.inf, 2), ("ungated", 0.5, 0), ("one", 1.0, 2),
+                         ("zero", 0.0, 2), ("neginf", -math.inf, 2)):
+        e = engine(name, 64)
+        e.ee_prefill(prompt)
+        out[key] = e.ee_decode_n_ex(tau, Le, 16, force_tokens=toks)
+    assert not out["inf"][1].any() and not out["one"][1].any()
+    assert out["zero"][1].all() and out["neginf"][1].all()
+    np.testing.assert_array_equal(out["inf"][0], out["ungated"][0])
+
+
+def test_persistent_and_per_op_agree_and_are_deterministic():
+    name = "tiny_bf16"
+    cfg = synth.get_config(name)
+    prompt = synth.prompts(cfg, 3, TINY_P)
+    tau = tiny_tau(name)
+    runs = []
+    for persistent in (True, True, False):
+        e = engine(name, 128, persistent)
+        e.ee_prefill(prompt)
+        d = [e.ee_decode_step_ex(tau, 2) for _ in range(6)]
+        runs.append(d)
+    for a, b in zip(runs[0], runs[1]):   # run twice: identical bytes
+        for k in ("token", "exited", "conf"):
+            assert a[k] == b[k]
+        for k in ("h_exit", "logits_readout"):
+            np.testing.assert_array_equal(a[k], b[k])
+    for a, b in zip(runs[0], runs[2]):   # same arithmetic per row in both programs
+        assert a["token"] == b["token"] and a["exited"] == b["exited"]
+        np.testing.assert_array_equal(a["h_exit"], b["h_exit"])
+        np.testing.assert_array_equal(a["logits_readout"], b["logits_readout"])
+        assert abs(a["conf"] - b["conf"]) <= 1e-6
+
+
+@pytest.mark.parametrize("page_size", [1, 16, 64])
+def test_paging_ragged_prompts(page_size):
+    name = "tiny_bf16"
+    cfg = synth.get_config(name)
+    for P in (1, 17, 64, 65):
+        prompt = synth.prompts(cfg, 40 + P, P)
+        toks = synth.prompts(cfg, 41 + P, 6)
+        o = oracle_for(name, P + 6)
+        g0 = o.prefill(prompt)
+        e = engine(name, P + 6, page_size=page_size)
+        g = e.ee_prefill(prompt)
+        if o.last_prefill_stats[2] > MARGIN:
+            assert g == g0
+        lockstep(e, o, None, 0.5, 2, 6, force_tokens=toks)
+
+
+def test_calibration_matches_oracle():
+    from paper_2609_14144_amd import EE_CAL_EXIT_RATE, EE_CAL_MEDIAN
+    name = "tiny_bf16"
+    cfg = synth.get_config(name)
+    prompts = [synth.prompts(cfg, s, TINY_P) for s in range(100, 108)]
+    e = engine(name, 64)
+    tau_med = e.ee_calibrate_threshold(prompts, TINY_N, 2, EE_CAL_MEDIAN, 0.0)
+    assert abs(tau_med - tiny_tau(name)) <= 1e-4
+    confs = []
+    for p in prompts:
+        o = oracle_for(name, 64)
+        confs += [r.conf for r in o.generate(o.prefill(p), math.inf, 2, TINY_N)]
+    for rate in (0.0, 0.25, 0.9, 1.0):
+        t_gpu = e.ee_calibrate_threshold(prompts, TINY_N, 2, EE_CAL_EXIT_RATE, rate)
+        t_ref = oracle.tau_for_exit_rate(confs, rate)
+        if math.isinf(t_ref):
+            assert t_gpu == t_ref
+        else:
+            assert abs(t_gpu - t_ref) <= 1e-4
+    assert e.ee_position() == 0
+
+
+def test_long_context_attention():
+    """4000-position prompt: 63 attention splits per kv head, ragged tail."""
+    name = "tiny_bf16"
+    cfg = synth.get_config(name)
+    P = 4000
+    prompt = synth.prompts(cfg, 9, P)
+    o = oracle_for(name, P + 4)
+    g0 = o.prefill(prompt)
+    e = engine(name, P + 4, page_size=64)
+    g = e.ee_prefill(prompt)
+    if o.last_prefill_stats[2] > MARGIN:
+        assert g == g0
+    rep, _ = lockstep(e, o, g0, 0.5, 2, 4, force_exit=[0, 1, 0, 0])
+    print("long-context worst rel err", max(r for _, r in rep))
+
+
+# ---------------------------------------------------------------------------
+# full-size 1.5B-shaped decoder (28 layers, H=1536, 12/2 heads, F=8960, V=151936)
+# ---------------------------------------------------------------------------
+D15 = "d1p5b"
+
+
+@pytest.fixture(scope="module")
+def d15():
+    cfg = synth.get_config(D15)
+    w = weights_for(D15)
+    prompt = synth.prompts(cfg, 1, 512)
+    o = oracle_for(D15, 512 + 64)
+    g0 = o.prefill(prompt)
+    return cfg, w, prompt, o, g0
+
+
+def test_d1p5b_lockstep_full_size(d15):
+    cfg, w, prompt, o, g0 = d15
+    o.reset()
+    assert o.prefill(prompt) == g0
+    e = engine(D15, 512 + 64)
+    assert e.ee_prefill(prompt) == g0 or o.last_prefill_stats[2] <= MARGIN
+    k, v = e.ee_read_kv(27, 511)
+    assert rel(k, o.kcache[27, 511].reshape(-1)) < 1e-2
+    rep, outside = lockstep(e, o, g0, 0.3, 14, 8)
+    print("1.5B lockstep worst rel err", max(r for _, r in rep), "outside-margin steps", outside)
+
+
+def test_d1p5b_decode_n_imposed_exits(d15):
+    """The timed entry point at full size: 16 steps in one launch with the
+    oracle's tokens and imposed branches (exit rate 0.5)."""
+    cfg, w, prompt, o, g0 = d15
+    o.reset()
+    o.prefill(prompt)
+    toks = synth.prompts(cfg, 8, 16)
+    fe = (np.arange(16) % 2).astype(np.int32)
+    rs = o.generate(None, 0.3, 14, 16, force_tokens=toks, force_exit=fe)
+    e = engine(D15, 512 + 64)
+    e.ee_prefill(prompt)
+    tok, ex, conf, would = e.ee_decode_n_ex(0.3, 14, 16, force_tokens=toks, force_exit=fe)
+    for i, r in enumerate(rs):
+        assert ex[i] == bool(fe[i])
+        assert abs(conf[i] - r.conf) <= 1e-4 + 1e-3 * r.conf
+        if abs(r.conf - 0.3) > MARGIN:
+            assert would[i] == r.would_exit
+        gap = r.gap_readout if r.exited else r.gap_full
+        if gap > MARGIN:
+            assert tok[i] == r.token, i
+
+
+def test_d1p5b_properties():
+    """Properties at full size: tau=+inf equals the ungated model token for
+    token; tau<=0 exits always; both device programs give the same tokens."""
+    cfg = synth.get_config(D15)
+    prompt = synth.prompts(cfg, 2, 512)
+    res = {}
+    for key, tau, Le, pers in (("inf", math.inf, 14, True), ("ungated", 0.5, 0, True),
+                               ("zero", 0.0, 14, True), ("inf_perop", math.inf, 14, False)):
+        e = engine(D15, 512 + 32, pers)
+        e.ee_prefill(prompt)
+        res[key] = e.ee_decode_n(tau, Le, 24)
+        e.close()
+    np.testing.assert_array_equal(res["inf"][0], res["ungated"][0])
+    np.testing.assert_array_equal(res["inf"][0], res["inf_perop"][0])
+    assert not res["inf"][1].any() and res["zero"][1].all()
+
+
+def test_head_kernel_planted_ties_full_vocab():
+    """The fused head at V=151936: planted exact ties resolve to the lowest
+    token id; argmax and max-probability match the oracle's head."""
+    cfg = synth.ModelConfig("headprobe", 1, 1536, 12, 2, 128, 512, 151936, "bf16", (1,))
+    w = synth.generate_weights(cfg)
+    o = oracle.OracleDecoder(cfg, w, 4)
+    x = np.random.default_rng(3).standard_normal(cfg.hidden).astype(np.float32)
+    lg = o.full_logits(x.astype(np.float64))
+    j = int(np.argmax(lg))
+    for k in (0, j // 2, max(0, j - 1)):
+        if k < j:
+            w["embed"][k] = w["embed"][j]       # exact tie with the maximum at a lower id
+            break
+    o = oracle.OracleDecoder(cfg, w, 4)
+    e = engine(None, 4, cfg=cfg, weights=w)
+    for layer in (0, 1):
+        if layer == 0:
+            ref = o.full_logits(x.astype(np.float64))
+        else:
+            ref = o.readout_logits(x.astype(np.float64), 1)
+        rj, rc, rg = oracle.head_stats(ref)
+        tok, conf, logits = e.ee_head_eval(layer, x)
+        assert rel(logits, ref) < 1e-4
+        assert abs(conf - rc) <= 1e-5 + 1e-4 * rc
+        if layer == 0:
+            assert rg == 0.0 and tok == rj  # the planted tie: lowest id wins
+        elif rg > MARGIN:
+            assert tok == rj
