@@ -5,7 +5,7 @@ Workload: the 1.5B-shaped decoder (28 layers, H=1536, 12 query / 2 KV heads
 of 128, SwiGLU F=8960, V=151936, tied embeddings, bf16 weights with fp32
 accumulation), readout at layer 14, a 512-token random prompt, then decode
 steps. The threshold tau is calibrated on the GPU (ee_calibrate_threshold)
-from 16 seeded 512-token prompts x 128 full-depth steps to target exit rates
+from 8 seeded 512-token prompts x 64 full-depth steps to target exit rates
 0.5 (the headline `value`), 0 and 0.96; the ungated model is timed too.
 
 A step is one decode step (one token) through the whole gated path. W
@@ -114,9 +114,11 @@ def cpu_baseline(cfg, w, prompt, tau, exit_layer, seconds):
     except Exception:
         threads = len(os.sched_getaffinity(0))
     o = oracle.OracleDecoder(cfg, w, PROMPT + 256)
+    log("cpu baseline: oracle built")
     t = time.perf_counter()
     tok = o.prefill(prompt)
     prefill_s = time.perf_counter() - t
+    log(f"cpu baseline: prefill {prefill_s:.1f}s")
     n = 0
     exits = 0
     t = time.perf_counter()
@@ -126,6 +128,8 @@ def cpu_baseline(cfg, w, prompt, tau, exit_layer, seconds):
         exits += r.exited
         n += 1
         el = time.perf_counter() - t
+        if n % 8 == 0:
+            log(f"cpu baseline: {n} steps in {el:.1f}s")
         if (el >= seconds and n >= 4) or n >= 256:
             break
     return {"value": n / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
@@ -141,8 +145,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=32)
     ap.add_argument("--config", default="d1p5b")
     ap.add_argument("--exit-layer", type=int, default=None, help="default: half depth")
-    ap.add_argument("--cal-prompts", type=int, default=16)
-    ap.add_argument("--cal-gen", type=int, default=128)
+    ap.add_argument("--cal-prompts", type=int, default=8)
+    ap.add_argument("--cal-gen", type=int, default=64)
     ap.add_argument("--program", choices=["persistent", "per_op"], default="persistent")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -182,7 +186,7 @@ def main():
     t = time.perf_counter()
     for r in rates:
         taus[r] = e.ee_calibrate_threshold(cal, args.cal_gen, Le, EE_CAL_EXIT_RATE, r)
-    log(f"calibrated tau {taus} in {time.perf_counter() - t:.1f}s")
+        log(f"calibrated tau for exit rate {r}: {taus[r]:.4g} ({time.perf_counter() - t:.1f}s)")
 
     prompt = synth.prompts(cfg, 1, PROMPT)
     # warm the code path once on another prompt

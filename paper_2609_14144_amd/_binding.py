@@ -228,8 +228,10 @@ class Engine:
         self._check(lib.ee_read_kv(self._ctx, layer, pos, _ptr(k, C.c_float), _ptr(v, C.c_float)))
         return k, v
 
-    def ee_set_persistent(self, on: bool):
-        self._check(lib.ee_set_persistent(self._ctx, 1 if on else 0))
+    def ee_set_persistent(self, wgs_per_cu):
+        """0/False: one kernel per operation; n >= 1 (True = 1): persistent kernel
+        with n workgroups per compute unit."""
+        self._check(lib.ee_set_persistent(self._ctx, int(wgs_per_cu)))
 
     def ee_last_decode_ms(self) -> float:
         ms = C.c_float()

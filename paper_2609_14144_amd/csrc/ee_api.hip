@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <map>
 #include <new>
 #include <random>
@@ -66,15 +67,33 @@ struct ee_ctx {
   bool persistent = true;
   int head_wgs = 0;
   int nwg_persistent = 0;
+  int max_wgs_per_cu = 0;
   size_t lds = 0;
   hipEvent_t ev0 = nullptr, ev1 = nullptr;
   float last_ms = 0.f;
+  int slot = -1;                       // constant-memory parameter slot (persistent kernel)
+  DevParams* params_pinned = nullptr;  // staging of the parameter block
   std::string err;
 };
 
 namespace {
 
 thread_local std::string g_create_err;  // last ee_create failure (no context exists)
+std::atomic<uint32_t> g_slots{0};       // parameter slots in use (one bit each)
+
+int take_slot() {
+  uint32_t cur = g_slots.load();
+  while (true) {
+    int i = 0;
+    while (i < ee::kParamSlots && (cur >> i & 1u)) ++i;
+    if (i == ee::kParamSlots) return -1;
+    if (g_slots.compare_exchange_weak(cur, cur | (1u << i))) return i;
+  }
+}
+
+void give_slot(int i) {
+  if (i >= 0) g_slots.fetch_and(~(1u << i));
+}
 
 int fail(ee_ctx* c, int code, const std::string& msg) {
   if (c) c->err = msg;
@@ -258,13 +277,15 @@ int run_steps(ee_ctx* c, float tau, int exit_layer, int n, const int32_t* d_forc
                            offsetof(ee::StepCtl, pad) - offsetof(ee::StepCtl, exited), c->stream));
   HIPCHK(c, hipEventRecord(c->ev0, c->stream));
   hipError_t e;
-  const bool pers = c->persistent && c->nwg_persistent > 0;
-  if (prefill) {
-    e = pers ? ee::launch_prefill_persistent(p, c->wbf16, c->pos, n, c->nwg_persistent, c->lds, c->stream)
-             : ee::launch_prefill_per_op(p, c->wbf16, c->pos, d_force_tok, n, c->head_wgs, c->stream);
+  const bool pers = c->persistent && c->nwg_persistent > 0 && c->slot >= 0;
+  if (pers) {
+    *c->params_pinned = p;
+    const ee::PersistentLaunch L{c->params_pinned, c->slot, c->wbf16, c->nwg_persistent, c->lds, c->stream};
+    e = prefill ? ee::launch_prefill_persistent(L, c->pos, n) : ee::launch_decode_persistent(L, c->pos, n);
+  } else if (prefill) {
+    e = ee::launch_prefill_per_op(p, c->wbf16, c->pos, d_force_tok, n, c->head_wgs, c->stream);
   } else {
-    e = pers ? ee::launch_decode_persistent(p, c->wbf16, c->pos, n, c->nwg_persistent, c->lds, c->stream)
-             : ee::launch_decode_per_op(p, c->wbf16, c->pos, n, c->head_wgs, c->stream);
+    e = ee::launch_decode_per_op(p, c->wbf16, c->pos, n, c->head_wgs, c->stream);
   }
   if (e != hipSuccess) return hip_fail(c, e, "kernel launch");
   HIPCHK(c, hipEventRecord(c->ev1, c->stream));
@@ -531,9 +552,23 @@ int ee_create(const ee_config* cfg, void* hip_stream, ee_ctx** out) {
 
   DevParams p = make_params(c, INFINITY, 0);
   c->lds = ee::lds_bytes(p);
-  const int per_cu = ee::persistent_max_wgs_per_cu(c->wbf16, c->lds);
-  c->nwg_persistent = per_cu > 0 ? c->n_cu * std::min(per_cu, 2) : 0;
-  c->head_wgs = 4 * c->n_cu;
+  const int cpl = ee::chunks_per_lane(p, c->wbf16);
+  if (cpl > (c->wbf16 ? 4 : 2)) {
+    c->err = "hidden too large for the compiled kernels (bf16: H <= 2048, fp32: H <= 512)";
+    return bail(EE_EINVAL);
+  }
+  if (c->lds > 64 * 1024) {
+    c->err = "shape needs more than 64 KB of LDS per workgroup";
+    return bail(EE_EINVAL);
+  }
+  c->max_wgs_per_cu = ee::persistent_max_wgs_per_cu(p, c->wbf16, c->lds);
+  c->slot = take_slot();
+  if ((he = hipHostMalloc(reinterpret_cast<void**>(&c->params_pinned), sizeof(DevParams))) != hipSuccess)
+    return bail(hip_fail(c, he, "hipHostMalloc parameter block"));
+  // without a free parameter slot the context uses the one-kernel-per-operation program
+  c->nwg_persistent = (c->max_wgs_per_cu > 0 && c->slot >= 0) ? c->n_cu : 0;
+  c->persistent = c->nwg_persistent > 0;
+  c->head_wgs = 2 * c->n_cu;
   c->max_parts = std::max(c->head_wgs, c->nwg_persistent);
   if ((r = dalloc(c, &c->d_head_part, static_cast<size_t>(c->max_parts) * 4 * 4))) return bail(r);
   *out = c;
@@ -749,12 +784,20 @@ int ee_read_kv(ee_ctx* c, int32_t layer, int32_t pos, float* k_out, float* v_out
   return EE_OK;
 }
 
-int ee_set_persistent(ee_ctx* c, int32_t on) {
+int ee_set_persistent(ee_ctx* c, int32_t wgs_per_cu) {
   if (!c) return EE_EINVAL;
   c->err.clear();
-  if (on && c->nwg_persistent <= 0)
-    return fail(c, EE_ESTATE, "persistent kernel cannot be co-resident on this device");
-  c->persistent = on != 0;
+  if (wgs_per_cu < 0) return fail(c, EE_EINVAL, "wgs_per_cu must be >= 0");
+  if (wgs_per_cu == 0) {
+    c->persistent = false;
+    return EE_OK;
+  }
+  if (wgs_per_cu > c->max_wgs_per_cu)
+    return fail(c, EE_EINVAL, "at most " + std::to_string(c->max_wgs_per_cu) +
+                                  " persistent workgroups per CU can be co-resident");
+  if (c->slot < 0) return fail(c, EE_ESTATE, "no free persistent-kernel parameter slot");
+  c->persistent = true;
+  c->nwg_persistent = c->n_cu * wgs_per_cu;
   return EE_OK;
 }
 
@@ -806,6 +849,8 @@ void ee_destroy(ee_ctx* c) {
   if (c->ev0) (void)hipEventDestroy(c->ev0);
   if (c->ev1) (void)hipEventDestroy(c->ev1);
   if (c->own_stream && c->stream) (void)hipStreamDestroy(c->stream);
+  if (c->params_pinned) (void)hipHostFree(c->params_pinned);
+  give_slot(c->slot);
   delete c;
 }
 

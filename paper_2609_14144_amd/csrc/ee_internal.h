@@ -9,9 +9,11 @@ namespace ee {
 
 constexpr int kWG = 256;               // threads per workgroup, every kernel
 constexpr int kWaves = kWG / 64;       // 64-wide wavefronts per workgroup
-constexpr int kAttnSplit = 64;         // positions per attention work item
+constexpr int kAttnSplit = kWaves * 64;  // positions per attention work item (64 per wave)
 constexpr int kMaxGroup = 8;           // max query heads per KV head
 constexpr int kMaxHeadDim = 256;
+constexpr int kBarGroups = 8;          // first level of the grid barrier (one per XCD)
+constexpr int kParamSlots = 16;        // persistent-kernel parameter blocks per device
 
 // Per-layer device pointers, repacked layouts:
 //   wqkv [(A + 2K) * D][H]: q rows, then k rows, then v rows. Within every q
@@ -47,9 +49,14 @@ struct StepCtl {
 enum : int32_t { kErrNone = 0, kErrBarrier = 1, kErrToken = 2 };
 
 // Grid barrier / last-arriver counters. Each lives on its own 256-byte line.
+// Barrier: workgroup wg arrives on group[wg % 8]; the last arrival of a group
+// arrives on top; the last arrival on top publishes the barrier's epoch in
+// gen, which every workgroup polls.
 struct Counters {
-  uint32_t barrier[64];
-  uint32_t attn[64 * 16];   // per KV head (index kvh * 64)
+  uint32_t group[kBarGroups][64];
+  uint32_t top[64];
+  uint32_t gen[64];
+  uint32_t attn[16][64];    // per KV head
   uint32_t head[64];
 };
 
@@ -104,15 +111,24 @@ struct DevParams {
 // Host launchers (defined in ee_kernels.hip).
 hipError_t launch_decode_per_op(const DevParams& p, int wbf16, int pos0, int n, int head_wgs,
                                 hipStream_t s);
-hipError_t launch_decode_persistent(const DevParams& p, int wbf16, int pos0, int n, int nwg,
-                                    size_t lds, hipStream_t s);
+// One persistent launch: the parameter block (pinned host memory) is copied
+// into constant-memory slot `slot` on `stream` before the kernel starts.
+struct PersistentLaunch {
+  const DevParams* params_host;
+  int slot;
+  int wbf16;
+  int nwg;
+  size_t lds;
+  hipStream_t stream;
+};
+hipError_t launch_decode_persistent(const PersistentLaunch& L, int pos0, int n);
 hipError_t launch_prefill_per_op(const DevParams& p, int wbf16, int pos0, const int32_t* d_tokens,
                                  int n, int head_wgs, hipStream_t s);
-hipError_t launch_prefill_persistent(const DevParams& p, int wbf16, int pos0, int n, int nwg,
-                                     size_t lds, hipStream_t s);
+hipError_t launch_prefill_persistent(const PersistentLaunch& L, int pos0, int n);
 hipError_t launch_head_eval(const DevParams& p, int wbf16, const float* d_x, int readout,
                             int head_wgs, hipStream_t s);
 size_t lds_bytes(const DevParams& p);
-int persistent_max_wgs_per_cu(int wbf16, size_t lds);
+int chunks_per_lane(const DevParams& p, int wbf16);
+int persistent_max_wgs_per_cu(const DevParams& p, int wbf16, size_t lds);
 
 }  // namespace ee

@@ -29,6 +29,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "ee_internal.h"
 
 namespace ee {
@@ -108,6 +110,11 @@ struct Elem<float> {
   __device__ static inline void store_pair(float* p, float a, float b) { st_coh2(p, a, b); }
 };
 
+__device__ __forceinline__ uint64_t ld_coh_u64(const void* p) {
+  return __hip_atomic_load(static_cast<uint64_t*>(const_cast<void*>(p)), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // ---------------------------------------------------------------------------
 // reductions
 // ---------------------------------------------------------------------------
@@ -145,31 +152,52 @@ __device__ inline float block_sum(float v, float* red) {
   return s;
 }
 
-// xs[i] = x[i] / sqrt(mean(x^2) + eps) * g[i]  (x fp32, written by other workgroups)
-__device__ inline void rmsnorm_to_lds(const float* x, const float* __restrict__ g, int n, float eps,
-                                      float* xs, float* red) {
-  __syncthreads();  // xs may still be read by a previous item
-  float ss = 0.f;
-  for (int i = threadIdx.x; i < n; i += kWG) {
-    const float v = ld_coh(x + i);
-    xs[i] = v;
-    ss = fmaf(v, v, ss);
+// ---------------------------------------------------------------------------
+// staging of activation vectors (written by other workgroups) into LDS:
+// coherent 8-byte loads, up to 8 per thread in flight. n is even.
+// ---------------------------------------------------------------------------
+__device__ inline void stage_coh(const float* x, int n, float* xs) {
+  const int n2 = n >> 1;
+  uint64_t* dst = reinterpret_cast<uint64_t*>(xs);
+  for (int base = 0; base < n2; base += 8 * kWG) {
+    uint64_t v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int i = base + k * kWG + static_cast<int>(threadIdx.x);
+      v[k] = i < n2 ? ld_coh_u64(x + 2 * i) : 0ull;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int i = base + k * kWG + static_cast<int>(threadIdx.x);
+      if (i < n2) dst[i] = v[k];
+    }
   }
+}
+
+// xs[i] = x[i] * rsqrt(mean(x^2) + eps) * (g ? g[i] : 1)
+__device__ inline void rmsnorm_stage(const float* x, const float* __restrict__ g, int n, float eps,
+                                     float* xs, float* red) {
+  __syncthreads();  // xs may still be read by a previous phase
+  stage_coh(x, n, xs);
+  __syncthreads();  // elements are staged in pairs by other threads
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < n; i += kWG) ss = fmaf(xs[i], xs[i], ss);
   const float r = rsqrtf(block_sum(ss, red) / static_cast<float>(n) + eps);
-  for (int i = threadIdx.x; i < n; i += kWG) xs[i] = xs[i] * r * g[i];
+  for (int i = threadIdx.x; i < n; i += kWG) xs[i] = xs[i] * r * (g ? g[i] : 1.f);
   __syncthreads();
 }
 
-__device__ inline void copy_to_lds(const float* x, int n, float* xs) {
+__device__ inline void copy_stage(const float* x, int n, float* xs) {
   __syncthreads();
-  for (int i = threadIdx.x; i < n; i += kWG) xs[i] = ld_coh(x + i);
+  stage_coh(x, n, xs);
   __syncthreads();
 }
 
 // ---------------------------------------------------------------------------
-// GEMV core: acc[r] += sum over 16-byte chunks c in [c0 + lane, c1) step 64 of
-// W[row r][chunk c] . xs[chunk c]. Rows beyond nvalid re-read the last valid
-// row (results discarded by the caller), so no access leaves the matrix.
+// GEMV building block: R rows x CPL 16-byte chunks per lane held in
+// registers. Lane `lane` owns chunks c0 + lane + 64k (k < CPL) below c1 of
+// each row. load() issues every load before anything waits on them, so a wave
+// can start fetching the next phase's weights before a grid barrier.
 // ---------------------------------------------------------------------------
 template <int N>
 __device__ inline void load_x(const float* xs, int c, float* x) {
@@ -192,40 +220,109 @@ __device__ inline float fma_chunk(const uint4& w, const float* x, float acc) {
   return acc;
 }
 
-template <typename WT, int R>
-__device__ inline void rows_dot(const WT* __restrict__ W, int64_t ld, int nvalid,
-                                const float* __restrict__ xs, int c0, int c1, int lane,
-                                float (&acc)[R]) {
-  constexpr int N = Elem<WT>::N;
-  const uint4* wr[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r)
-    wr[r] = reinterpret_cast<const uint4*>(W + static_cast<int64_t>(r < nvalid ? r : nvalid - 1) * ld);
-  int c = c0 + lane;
-  for (; c + 64 < c1; c += 128) {
-    uint4 w0[R], w1[R];
+template <typename WT, int R, int CPL>
+struct RowBlock {
+  static constexpr int N = Elem<WT>::N;
+  uint4 w[R][CPL];
+
+  __device__ __forceinline__ void load(const WT* W, int64_t ld, int row0, int nr, int c0, int c1) {
+    const int lane = threadIdx.x & 63;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
-      w0[r] = wr[r][c];
-      w1[r] = wr[r][c + 64];
-    }
-    float x0[N], x1[N];
-    load_x<N>(xs, c, x0);
-    load_x<N>(xs, c + 64, x1);
+      const uint4* row = reinterpret_cast<const uint4*>(W + static_cast<int64_t>(row0 + r) * ld);
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      acc[r] = fma_chunk<WT>(w0[r], x0, acc[r]);
-      acc[r] = fma_chunk<WT>(w1[r], x1, acc[r]);
+      for (int k = 0; k < CPL; ++k) {
+        const int c = c0 + lane + 64 * k;
+        w[r][k] = (r < nr && c < c1) ? row[c] : make_uint4(0u, 0u, 0u, 0u);
+      }
     }
   }
-  if (c < c1) {
-    uint4 w0[R];
+
+  // acc[r] = W[row r] . xs over this lane's chunks (partial: reduce over lanes after)
+  __device__ __forceinline__ void dot(const float* xs, int nr, int c0, int c1, float (&acc)[R]) const {
+    const int lane = threadIdx.x & 63;
 #pragma unroll
-    for (int r = 0; r < R; ++r) w0[r] = wr[r][c];
-    float x0[N];
-    load_x<N>(xs, c, x0);
+    for (int r = 0; r < R; ++r) acc[r] = 0.f;
 #pragma unroll
-    for (int r = 0; r < R; ++r) acc[r] = fma_chunk<WT>(w0[r], x0, acc[r]);
+    for (int k = 0; k < CPL; ++k) {
+      const int c = c0 + lane + 64 * k;
+      if (c < c1) {
+        float x[N];
+        load_x<N>(xs, c, x);
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+          if (r < nr) acc[r] = fma_chunk<WT>(w[r][k], x, acc[r]);
+      }
+    }
+  }
+
+  // as dot(), with x scaled elementwise by g (global, read-only)
+  __device__ __forceinline__ void dot_gain(const float* xs, const float* __restrict__ g, int nr, int c0,
+                                           int c1, float (&acc)[R]) const {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int r = 0; r < R; ++r) acc[r] = 0.f;
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) {
+      const int c = c0 + lane + 64 * k;
+      if (c < c1) {
+        float x[N];
+        load_x<N>(xs, c, x);
+#pragma unroll
+        for (int e = 0; e < N; ++e) x[e] *= g[c * N + e];
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+          if (r < nr) acc[r] = fma_chunk<WT>(w[r][k], x, acc[r]);
+      }
+    }
+  }
+};
+
+// Tiles of R rows x (at most 64*CPL) chunks covering rows [rb, re) and chunk
+// range [cb, ce), row block by row block, double buffered: tile t+1 is loaded
+// before tile t is consumed. Tile 0 must be loaded into `a` already (typically
+// before a grid barrier wait). np = pieces per row block (the same for every
+// wave that shares the row blocks). emit(row0, nrows, acc) receives each row
+// block's wave-reduced dot products over [cb, ce).
+template <typename WT, int R, int CPL>
+struct Tiling {
+  int rb, re, cb, ce, np;
+  __device__ __forceinline__ int count() const { return ((re - rb + R - 1) / R) * np; }
+  __device__ __forceinline__ int row(int t) const { return rb + (t / np) * R; }
+  __device__ __forceinline__ int nrows(int t) const { return min(R, re - row(t)); }
+  __device__ __forceinline__ int c0(int t) const { return cb + (t % np) * 64 * CPL; }
+  __device__ __forceinline__ int c1(int t) const { return min(ce, c0(t) + 64 * CPL); }
+  __device__ __forceinline__ void load(RowBlock<WT, R, CPL>& blk, const WT* W, int64_t ld, int t) const {
+    blk.load(W, ld, row(t), nrows(t), c0(t), c1(t));
+  }
+};
+
+template <typename WT, int R, int CPL, typename Emit>
+__device__ __forceinline__ void stream_tiles(const WT* W, int64_t ld, const Tiling<WT, R, CPL>& tl,
+                                             const float* xs, RowBlock<WT, R, CPL>& a,
+                                             RowBlock<WT, R, CPL>& b, Emit&& emit) {
+  const int nt = tl.count();
+  float tot[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) tot[r] = 0.f;
+  auto consume = [&](const RowBlock<WT, R, CPL>& blk, int t) {
+    float acc[R];
+    blk.dot(xs, tl.nrows(t), tl.c0(t), tl.c1(t), acc);
+#pragma unroll
+    for (int r = 0; r < R; ++r) tot[r] += acc[r];
+    if (t % tl.np == tl.np - 1) {
+      wave_sum_n<R>(tot);
+      emit(tl.row(t), tl.nrows(t), tot);
+#pragma unroll
+      for (int r = 0; r < R; ++r) tot[r] = 0.f;
+    }
+  };
+  for (int t = 0; t < nt; t += 2) {
+    if (t + 1 < nt) tl.load(b, W, ld, t + 1);
+    consume(a, t);
+    if (t + 1 >= nt) break;
+    if (t + 2 < nt) tl.load(a, W, ld, t + 2);
+    consume(b, t + 1);
   }
 }
 
@@ -279,17 +376,29 @@ __device__ inline int step_token(const DevParams& p, int step) {
   return tok;
 }
 
+__device__ __forceinline__ int wave_id() { return static_cast<int>(threadIdx.x >> 6); }
+
 // ---------------------------------------------------------------------------
-// phase: RMSNorm + QKV projection + RoPE + KV append (one layer)
-// For layer 0 the input is the embedding row of the step's token, and
-// workgroup 0 also initialises the residual stream h with it.
+// phase: RMSNorm + QKV projection + RoPE + KV append (one layer). Global wave
+// gw owns row pair gw (+ total waves while rows remain). For layer 0 the input
+// is the embedding row of the step's token, and workgroup 0 also initialises
+// the residual stream h with it.
 // ---------------------------------------------------------------------------
-template <typename WT>
+template <typename WT, int CPL>
+struct QkvTask {
+  RowBlock<WT, 2, CPL> blk;
+  __device__ __forceinline__ void prefetch(const DevParams& p, int l, int wg) {
+    const int pair = wg * kWaves + wave_id();
+    blk.load(static_cast<const WT*>(p.layers[l].wqkv), p.H, 2 * pair, pair < (p.qkv_rows >> 1) ? 2 : 0,
+             0, p.H / Elem<WT>::N);
+  }
+};
+
+template <typename WT, int CPL>
 __device__ void phase_qkv(const DevParams& p, int l, int pos, int step, int wg, int nwg, float* xs,
-                          float* red) {
+                          float* red, QkvTask<WT, CPL>& t) {
   const int pairs = p.qkv_rows >> 1;
-  const int items = (pairs + kWaves - 1) / kWaves;
-  if (wg >= items) return;
+  if (wg * kWaves >= pairs) return;
   const LayerW lw = p.layers[l];
   if (l == 0) {
     const int tok = step_token(p, step);
@@ -307,32 +416,34 @@ __device__ void phase_qkv(const DevParams& p, int l, int pos, int step, int wg, 
     __syncthreads();
     if (wg == 0 && threadIdx.x == 0) st_coh(&p.ctl->exited, 0);
   } else {
-    rmsnorm_to_lds(p.h, lw.g_attn, p.H, p.eps, xs, red);
+    rmsnorm_stage(p.h, lw.g_attn, p.H, p.eps, xs, red);
   }
-  const WT* W = static_cast<const WT*>(lw.wqkv);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int nch = p.H / Elem<WT>::N;
-  for (int it = wg; it < items; it += nwg) {
-    const int pair = it * kWaves + wave;
-    if (pair >= pairs) continue;
-    const int r0 = 2 * pair;
-    float acc[2] = {0.f, 0.f};
-    rows_dot<WT, 2>(W + static_cast<int64_t>(r0) * p.H, p.H, 2, xs, 0, nch, lane, acc);
+  const int tw = nwg * kWaves;
+  for (int pair = wg * kWaves + wave_id(); pair < pairs; pair += tw) {
+    if (pair != wg * kWaves + wave_id())
+      t.blk.load(static_cast<const WT*>(lw.wqkv), p.H, 2 * pair, 2, 0, nch);
+    float acc[2];
+    t.blk.dot(xs, 2, 0, nch, acc);
     wave_sum_n<2>(acc);
-    if (lane == 0) store_qkv_pair<WT>(p, l, pos, r0, acc[0], acc[1]);
+    if ((threadIdx.x & 63) == 0) store_qkv_pair<WT>(p, l, pos, 2 * pair, acc[0], acc[1]);
   }
 }
 
 // ---------------------------------------------------------------------------
-// phase: decode attention over positions 0..pos, grouped-query. A wave item
-// is (kv head, split of kAttnSplit = 64 positions). Scores: lanes own
-// positions (q of the G query heads sharing the kv head broadcast from LDS).
-// Weighted V: groups of D/N lanes own one position's row in 16-byte chunks.
-// Each item writes a partial (max, sum of exp, weighted V); the last item of a
-// kv head to finish merges the splits in index order into o.
+// phase: decode attention over positions 0..pos, grouped-query. Workgroup
+// item = (kv head, split of kAttnSplit positions); wave w of the item takes
+// 64 positions. Scores: lanes own positions (q of the G query heads sharing
+// the kv head broadcast from LDS). Weighted V: groups of D/N lanes read one
+// position's row in 16-byte chunks. The waves merge in LDS; with one split
+// the item writes o directly, otherwise it writes a partial (max, sum of exp,
+// weighted V) and the last split of the kv head merges in index order.
 // ---------------------------------------------------------------------------
+__host__ __device__ inline int attn_wave_floats(int G, int D) {
+  return 2 * 64 + G * 64 + G * D + 2 * G;  // offsets | exp(score) | weighted V | m, l
+}
 __host__ __device__ inline int attn_lds_floats(int G, int D) {
-  return kWaves * (G * D + G * kAttnSplit + 2 * kAttnSplit);
+  return G * D + kWaves * attn_wave_floats(G, D);
 }
 
 template <typename WT>
@@ -341,33 +452,35 @@ __device__ void phase_attn(const DevParams& p, int l, int pos, int wg, int nwg, 
   const int T = pos + 1;
   const int nsplit = (T + kAttnSplit - 1) / kAttnSplit;
   const int items = p.K * nsplit;
-  const int witems = (items + kWaves - 1) / kWaves;
-  if (wg >= witems) return;
+  if (wg >= items) return;
   const int G = p.G, D = p.D;
-  const int PS = D + 2;  // partial record: m, l, acc[D]
+  const int PS = D + 2;
   const int LPP = D / N, PPW = 64 / LPP;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = wave_id(), lane = threadIdx.x & 63;
   const int sub = lane / LPP, dl = lane - sub * LPP;
-  float* qw = lds + wave * (G * D + G * kAttnSplit + 2 * kAttnSplit);  // [G][D] scaled q
-  float* pw = qw + G * D;                                              // [G][64] exp(s - m)
-  int64_t* offw = reinterpret_cast<int64_t*>(pw + G * kAttnSplit);     // [64] row offsets
+  float* qs = lds;  // [G][D] scaled q
+  float* wb = lds + G * D + wave * attn_wave_floats(G, D);
+  int64_t* offw = reinterpret_cast<int64_t*>(wb);  // [64]
+  float* pw = wb + 128;                            // [G][64]
+  float* accw = pw + G * 64;                       // [G][D]
+  float* mlw = accw + G * D;                       // [G] m, [G] l
   const WT* kp = static_cast<const WT*>(p.kpool);
   const WT* vp = static_cast<const WT*>(p.vpool);
+  __shared__ int last_flag;
 
-  for (int wit = wg; wit < witems; wit += nwg) {
-    const int item = wit * kWaves + wave;
-    const bool active = item < items;
-    const int kvh = active ? item / nsplit : 0;
-    const int sp = active ? item - kvh * nsplit : 0;
-    const int s0 = sp * kAttnSplit;
-    const int ns = active ? min(kAttnSplit, T - s0) : 0;
-    __syncthreads();  // the previous item's LDS reads are done
-    if (active) {
-      for (int i = lane; i < G * D; i += 64) qw[i] = ld_coh(p.q + kvh * G * D + i) * p.attn_scale;
-      offw[lane] = lane < ns ? kv_offset(p, l, s0 + lane, kvh) : 0;
-    }
+  for (int it = wg; it < items; it += nwg) {
+    const int kvh = it / nsplit, sp = it - kvh * nsplit;
+    const int ws0 = sp * kAttnSplit + wave * 64;
+    const int wn = max(0, min(64, T - ws0));  // positions of this wave
     __syncthreads();
-    const bool valid = lane < ns;
+    for (int i = threadIdx.x * 2; i < G * D; i += kWG * 2) {
+      const uint64_t v = ld_coh_u64(p.q + kvh * G * D + i);
+      qs[i] = __uint_as_float(static_cast<uint32_t>(v)) * p.attn_scale;
+      qs[i + 1] = __uint_as_float(static_cast<uint32_t>(v >> 32)) * p.attn_scale;
+    }
+    if (lane < wn) offw[lane] = kv_offset(p, l, ws0 + lane, kvh);
+    __syncthreads();
+    const bool valid = lane < wn;
     float sc[kMaxGroup];
 #pragma unroll
     for (int g = 0; g < kMaxGroup; ++g) sc[g] = 0.f;
@@ -380,7 +493,7 @@ __device__ void phase_attn(const DevParams& p, int l, int pos, int wg, int nwg, 
 #pragma unroll
         for (int g = 0; g < kMaxGroup; ++g) {
           if (g < G) {
-            const float* qg = qw + g * D + c * N;
+            const float* qg = qs + g * D + c * N;
 #pragma unroll
             for (int e = 0; e < N; ++e) sc[g] = fmaf(qg[e], kf[e], sc[g]);
           }
@@ -390,187 +503,260 @@ __device__ void phase_attn(const DevParams& p, int l, int pos, int wg, int nwg, 
     float mg[kMaxGroup], lg[kMaxGroup];
 #pragma unroll
     for (int g = 0; g < kMaxGroup; ++g) {
-      mg[g] = 0.f;
+      mg[g] = -INFINITY;
       lg[g] = 0.f;
-      if (g < G) {
+      if (g < G && wn > 0) {
         const float v = valid ? sc[g] : -INFINITY;
         const float m = wave_max(v);
         const float e = valid ? expf(v - m) : 0.f;
         mg[g] = m;
         lg[g] = wave_sum(e);
-        if (active) pw[g * kAttnSplit + lane] = e;
+        pw[g * 64 + lane] = e;
       }
     }
     __syncthreads();
-    if (!active) continue;
-    // weighted V: lanes (sub, dl) take position j0 + sub, dimensions dl*N .. dl*N + N
-    float acc[kMaxGroup][N];
+    if (wn > 0) {
+      // query heads in groups of kVG to bound the accumulator registers
+      constexpr int kVG = 4;
+      for (int g0 = 0; g0 < G; g0 += kVG) {
+        float acc[kVG][N];
 #pragma unroll
-    for (int g = 0; g < kMaxGroup; ++g)
+        for (int g = 0; g < kVG; ++g)
 #pragma unroll
-      for (int e = 0; e < N; ++e) acc[g][e] = 0.f;
+          for (int e = 0; e < N; ++e) acc[g][e] = 0.f;
 #pragma unroll 2
-    for (int j0 = 0; j0 < ns; j0 += PPW) {
-      const int j = j0 + sub;
-      if (j < ns) {
-        const uint4 vw = *reinterpret_cast<const uint4*>(vp + offw[j] + dl * N);
-        float vf[N];
-        Elem<WT>::unpack(vw, vf);
+        for (int j0 = 0; j0 < wn; j0 += PPW) {
+          const int j = j0 + sub;
+          if (j < wn) {
+            const uint4 vw = *reinterpret_cast<const uint4*>(vp + offw[j] + dl * N);
+            float vf[N];
+            Elem<WT>::unpack(vw, vf);
+#pragma unroll
+            for (int g = 0; g < kVG; ++g) {
+              if (g0 + g < G) {
+                const float pj = pw[(g0 + g) * 64 + j];
+#pragma unroll
+                for (int e = 0; e < N; ++e) acc[g][e] = fmaf(pj, vf[e], acc[g][e]);
+              }
+            }
+          }
+        }
+        for (int off = LPP; off < 64; off <<= 1) {
+#pragma unroll
+          for (int g = 0; g < kVG; ++g)
+#pragma unroll
+            for (int e = 0; e < N; ++e) acc[g][e] += __shfl_xor(acc[g][e], off, 64);
+        }
+        if (sub == 0) {
+#pragma unroll
+          for (int g = 0; g < kVG; ++g)
+            if (g0 + g < G)
+#pragma unroll
+              for (int e = 0; e < N; ++e) accw[(g0 + g) * D + dl * N + e] = acc[g][e];
+        }
+      }
+      if (lane == 0) {
 #pragma unroll
         for (int g = 0; g < kMaxGroup; ++g) {
           if (g < G) {
-            const float pj = pw[g * kAttnSplit + j];
-#pragma unroll
-            for (int e = 0; e < N; ++e) acc[g][e] = fmaf(pj, vf[e], acc[g][e]);
+            mlw[g] = mg[g];
+            mlw[G + g] = lg[g];
           }
         }
       }
     }
-    for (int off = LPP; off < 64; off <<= 1) {
-#pragma unroll
-      for (int g = 0; g < kMaxGroup; ++g)
-        if (g < G)
-#pragma unroll
-          for (int e = 0; e < N; ++e) acc[g][e] += __shfl_xor(acc[g][e], off, 64);
-    }
+    __syncthreads();
+    // merge the waves of this item (fixed order)
+    const int nw = min(kWaves, (T - sp * kAttnSplit + 63) / 64);
     float* part = p.attn_part + (static_cast<int64_t>(kvh) * p.max_splits + sp) * G * PS;
-#pragma unroll
-    for (int g = 0; g < kMaxGroup; ++g) {
-      if (g < G) {
-        if (sub == 0) {
-#pragma unroll
-          for (int e = 0; e < N; e += 2)
-            st_coh2(part + g * PS + 2 + dl * N + e, acc[g][e], acc[g][e + 1]);
-        }
-        if (lane == 0) st_coh2(part + g * PS, mg[g], lg[g]);
+    const float* base0 = lds + G * D;
+    for (int idx = threadIdx.x; idx < G * D; idx += kWG) {
+      const int g = idx / D, d = idx - g * D;
+      float M = -INFINITY;
+      for (int w = 0; w < nw; ++w) {
+        const float* m = base0 + w * attn_wave_floats(G, D) + 128 + G * 64 + G * D;
+        M = fmaxf(M, m[g]);
       }
-    }
-    // the last item of this kv head to finish merges all splits into o
-    wait_stores();
-    uint32_t old = 0;
-    if (lane == 0)
-      old = __hip_atomic_fetch_add(&p.counters->attn[kvh * 64], 1u, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-    old = __shfl(old, 0, 64);
-    if (old == static_cast<uint32_t>(nsplit - 1)) {
-      const float* base = p.attn_part + static_cast<int64_t>(kvh) * p.max_splits * G * PS;
-      for (int idx = lane; idx < G * D; idx += 64) {
-        const int g = idx / D, d = idx - g * D;
-        float M = -INFINITY;
-        for (int s2 = 0; s2 < nsplit; ++s2) M = fmaxf(M, ld_coh(base + (s2 * G + g) * PS));
-        float den = 0.f, num = 0.f;
-        for (int s2 = 0; s2 < nsplit; ++s2) {
-          const float* rec = base + (s2 * G + g) * PS;
-          const float wgt = expf(ld_coh(rec) - M);
-          den = fmaf(wgt, ld_coh(rec + 1), den);
-          num = fmaf(wgt, ld_coh(rec + 2 + d), num);
-        }
+      float den = 0.f, num = 0.f;
+      for (int w = 0; w < nw; ++w) {
+        const float* wb2 = base0 + w * attn_wave_floats(G, D);
+        const float* ml = wb2 + 128 + G * 64 + G * D;
+        const float f = expf(ml[g] - M);
+        den = fmaf(f, ml[G + g], den);
+        num = fmaf(f, wb2[128 + G * 64 + g * D + d], num);
+      }
+      if (nsplit == 1) {
         st_coh(p.o + (kvh * G + g) * D + d, num / den);
-      }
-      if (lane == 0)
-        __hip_atomic_store(&p.counters->attn[kvh * 64], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// phase: out[r] (+)= W[r] . x for rows of a [rows][cols] matrix, x staged in
-// LDS. Items of kWaves * R rows, one R-row group per wave.
-// mode 0: out = acc + bias (bias may be null); mode 1: out += acc.
-// ---------------------------------------------------------------------------
-template <typename WT, int R>
-__device__ void phase_gemv(const WT* __restrict__ W, int rows, int cols, const float* x, float* out,
-                           const float* bias, int mode, int wg, int nwg, float* xs) {
-  const int items = (rows + kWaves * R - 1) / (kWaves * R);
-  if (wg >= items) return;
-  copy_to_lds(x, cols, xs);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int nch = cols / Elem<WT>::N;
-  for (int it = wg; it < items; it += nwg) {
-    const int r0 = (it * kWaves + wave) * R;
-    if (r0 >= rows) continue;
-    const int nv = min(R, rows - r0);
-    float acc[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) acc[r] = 0.f;
-    rows_dot<WT, R>(W + static_cast<int64_t>(r0) * cols, cols, nv, xs, 0, nch, lane, acc);
-    wave_sum_n<R>(acc);
-    if (lane == 0) {
-      for (int r = 0; r < nv; ++r) {
-        const float prev = mode == 1 ? ld_coh(out + r0 + r) : (bias ? bias[r0 + r] : 0.f);
-        st_coh(out + r0 + r, prev + acc[r]);
+      } else {
+        st_coh(part + g * PS + 2 + d, num);
+        if (d == 0) st_coh2(part + g * PS, M, den);
       }
     }
+    if (nsplit == 1) continue;
+    // the last split of this kv head to finish merges all splits into o
+    wait_stores();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      const uint32_t old = __hip_atomic_fetch_add(&p.counters->attn[kvh][0], 1u, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+      last_flag = (old == static_cast<uint32_t>(nsplit - 1));
+    }
+    __syncthreads();
+    if (!last_flag) continue;
+    const float* base = p.attn_part + static_cast<int64_t>(kvh) * p.max_splits * G * PS;
+    for (int idx = threadIdx.x; idx < G * D; idx += kWG) {
+      const int g = idx / D, d = idx - g * D;
+      float M = -INFINITY;
+      for (int s2 = 0; s2 < nsplit; ++s2) M = fmaxf(M, ld_coh(base + (s2 * G + g) * PS));
+      float den = 0.f, num = 0.f;
+#pragma unroll 4
+      for (int s2 = 0; s2 < nsplit; ++s2) {
+        const float* rec = base + (s2 * G + g) * PS;
+        const float f = expf(ld_coh(rec) - M);
+        den = fmaf(f, ld_coh(rec + 1), den);
+        num = fmaf(f, ld_coh(rec + 2 + d), num);
+      }
+      st_coh(p.o + (kvh * G + g) * D + d, num / den);
+    }
+    if (threadIdx.x == 0)
+      __hip_atomic_store(&p.counters->attn[kvh][0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
-// Same with the K dimension split over the workgroup's waves: item = R rows,
-// wave w handles chunk range w of kWaves; partial sums meet in LDS. out += acc.
-template <typename WT, int R>
-__device__ void phase_gemv_splitk(const WT* __restrict__ W, int rows, int cols, const float* x,
-                                  float* out, int wg, int nwg, float* xs, float* red) {
-  const int items = (rows + R - 1) / R;
-  if (wg >= items) return;
-  copy_to_lds(x, cols, xs);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+// ---------------------------------------------------------------------------
+// phase: one row per wave, out[r] = W[r] . x (+ bias) or out[r] += W[r] . x.
+// Used for Wo (residual) and the readout (bias).
+// ---------------------------------------------------------------------------
+template <typename WT, int CPL>
+struct RowTask {
+  RowBlock<WT, 1, CPL> blk;
+  __device__ __forceinline__ void prefetch(const WT* W, int rows, int cols, int wg) {
+    const int r = wg * kWaves + wave_id();
+    blk.load(W, cols, r, r < rows ? 1 : 0, 0, cols / Elem<WT>::N);
+  }
+};
+
+template <typename WT, int CPL>
+__device__ void phase_rows(const WT* W, int rows, int cols, const float* x, float* out,
+                           const float* bias, int residual, int wg, int nwg, float* xs,
+                           RowTask<WT, CPL>& t) {
+  if (wg * kWaves >= rows) return;
+  copy_stage(x, cols, xs);
   const int nch = cols / Elem<WT>::N;
-  const int cb = nch * wave / kWaves, ce = nch * (wave + 1) / kWaves;
-  for (int it = wg; it < items; it += nwg) {
-    const int r0 = it * R;
-    const int nv = min(R, rows - r0);
-    float acc[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) acc[r] = 0.f;
-    rows_dot<WT, R>(W + static_cast<int64_t>(r0) * cols, cols, nv, xs, cb, ce, lane, acc);
-    wave_sum_n<R>(acc);
-    if (lane == 0) {
-#pragma unroll
-      for (int r = 0; r < R; ++r) red[wave * R + r] = acc[r];
+  const int tw = nwg * kWaves;
+  for (int r = wg * kWaves + wave_id(); r < rows; r += tw) {
+    if (r != wg * kWaves + wave_id()) t.blk.load(W, cols, r, 1, 0, nch);
+    float acc[1];
+    t.blk.dot(xs, 1, 0, nch, acc);
+    acc[0] = wave_sum(acc[0]);
+    if ((threadIdx.x & 63) == 0) {
+      const float prev = residual ? ld_coh(out + r) : (bias ? bias[r] : 0.f);
+      st_coh(out + r, prev + acc[0]);
     }
-    __syncthreads();
-    if (threadIdx.x < nv) {
-      float s = 0.f;
-      for (int w = 0; w < kWaves; ++w) s += red[w * R + threadIdx.x];
-      st_coh(out + r0 + threadIdx.x, ld_coh(out + r0 + threadIdx.x) + s);
-    }
-    __syncthreads();
   }
 }
 
 // ---------------------------------------------------------------------------
-// phase: RMSNorm + gate/up projection + SiLU(gate) * up. Interleaved rows.
+// phase: RMSNorm + gate/up projection + SiLU(gate) * up. Interleaved rows
+// (2j = gate j, 2j+1 = up j). Global wave gw owns the contiguous output range
+// [gw F / W, (gw+1) F / W), streamed in blocks of two outputs.
 // ---------------------------------------------------------------------------
+constexpr int kRS = 2;  // rows per streamed block
+
+__device__ __forceinline__ int gu_begin(const DevParams& p, int gw, int tw) {
+  return static_cast<int>(static_cast<int64_t>(p.F) * gw / tw);
+}
+
+template <typename WT, int CPL>
+struct GateUpTask {
+  RowBlock<WT, kRS, CPL> a, b;
+  __device__ __forceinline__ static Tiling<WT, kRS, CPL> tiling(const DevParams& p, int wg, int nwg) {
+    const int tw = nwg * kWaves, gw = wg * kWaves + wave_id();
+    return Tiling<WT, kRS, CPL>{2 * gu_begin(p, gw, tw), 2 * gu_begin(p, gw + 1, tw), 0,
+                                p.H / Elem<WT>::N, 1};
+  }
+  __device__ __forceinline__ void prefetch(const DevParams& p, int l, int wg, int nwg) {
+    const auto tl = tiling(p, wg, nwg);
+    if (tl.count() > 0) tl.load(a, static_cast<const WT*>(p.layers[l].wgu), p.H, 0);
+  }
+};
+
 __device__ inline float silu(float x) { return x / (1.f + expf(-x)); }
 
-template <typename WT>
-__device__ void phase_gateup(const DevParams& p, int l, int wg, int nwg, float* xs, float* red) {
-  const int items = (p.F + 2 * kWaves - 1) / (2 * kWaves);
-  if (wg >= items) return;
+template <typename WT, int CPL>
+__device__ void phase_gateup(const DevParams& p, int l, int wg, int nwg, float* xs, float* red,
+                             GateUpTask<WT, CPL>& t) {
+  const int tw = nwg * kWaves;
+  const int gw0 = wg * kWaves;
+  if (gu_begin(p, gw0 + kWaves, tw) == gu_begin(p, gw0, tw)) return;
   const LayerW lw = p.layers[l];
-  rmsnorm_to_lds(p.h, lw.g_mlp, p.H, p.eps, xs, red);
-  const WT* W = static_cast<const WT*>(lw.wgu);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int nch = p.H / Elem<WT>::N;
-  for (int it = wg; it < items; it += nwg) {
-    const int j0 = (it * kWaves + wave) * 2;
-    if (j0 >= p.F) continue;
-    const int nv = min(4, 2 * (p.F - j0));
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
-    rows_dot<WT, 4>(W + static_cast<int64_t>(2 * j0) * p.H, p.H, nv, xs, 0, nch, lane, acc);
-    wave_sum_n<4>(acc);
-    if (lane == 0) {
-      if (nv == 4) st_coh2(p.a + j0, silu(acc[0]) * acc[1], silu(acc[2]) * acc[3]);
-      else st_coh(p.a + j0, silu(acc[0]) * acc[1]);
-    }
+  rmsnorm_stage(p.h, lw.g_mlp, p.H, p.eps, xs, red);
+  float* a_out = p.a;
+  stream_tiles<WT, kRS, CPL>(static_cast<const WT*>(lw.wgu), p.H, GateUpTask<WT, CPL>::tiling(p, wg, nwg),
+                             xs, t.a, t.b, [&](int r0, int nr, const float(&acc)[kRS]) {
+                              if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+                                for (int i = 0; i < kRS / 2; ++i)
+                                  if (2 * i < nr) st_coh(a_out + r0 / 2 + i, silu(acc[2 * i]) * acc[2 * i + 1]);
+                              }
+                            });
+}
+
+// ---------------------------------------------------------------------------
+// phase: h += W_d a. Workgroup wg owns rows [wg H / nwg, (wg+1) H / nwg); its
+// waves split the F dimension into kWaves contiguous chunk ranges and stream
+// tiles of kRS rows x 64*CPL chunks; per row block the partial sums of the
+// waves meet in LDS.
+// ---------------------------------------------------------------------------
+template <typename WT, int CPL>
+struct DownTask {
+  RowBlock<WT, kRS, CPL> a, b;
+  __device__ __forceinline__ static Tiling<WT, kRS, CPL> tiling(const DevParams& p, int wg, int nwg) {
+    const int nch = p.F / Elem<WT>::N;
+    const int longest = (nch + kWaves - 1) / kWaves;
+    return Tiling<WT, kRS, CPL>{static_cast<int>(static_cast<int64_t>(p.H) * wg / nwg),
+                                static_cast<int>(static_cast<int64_t>(p.H) * (wg + 1) / nwg),
+                                nch * wave_id() / kWaves, nch * (wave_id() + 1) / kWaves,
+                                max(1, (longest + 64 * CPL - 1) / (64 * CPL))};
   }
+  __device__ __forceinline__ void prefetch(const DevParams& p, int l, int wg, int nwg) {
+    const auto tl = tiling(p, wg, nwg);
+    if (tl.count() > 0) tl.load(a, static_cast<const WT*>(p.layers[l].wd), p.F, 0);
+  }
+};
+
+template <typename WT, int CPL>
+__device__ void phase_down(const DevParams& p, int l, int wg, int nwg, float* xs, float* red,
+                           DownTask<WT, CPL>& t) {
+  const auto tl = DownTask<WT, CPL>::tiling(p, wg, nwg);
+  if (tl.rb >= tl.re) return;
+  copy_stage(p.a, p.F, xs);
+  const int wave = wave_id();
+  float* h = p.h;
+  stream_tiles<WT, kRS, CPL>(static_cast<const WT*>(p.layers[l].wd), p.F, tl, xs, t.a, t.b,
+                             [&](int r0, int nr, const float(&acc)[kRS]) {
+                               if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+                                 for (int i = 0; i < kRS; ++i) red[wave * kRS + i] = acc[i];
+                               }
+                               __syncthreads();
+                               if (static_cast<int>(threadIdx.x) < nr) {
+                                 float sum = 0.f;
+                                 for (int w = 0; w < kWaves; ++w) sum += red[w * kRS + threadIdx.x];
+                                 st_coh(h + r0 + threadIdx.x, ld_coh(h + r0 + threadIdx.x) + sum);
+                               }
+                               __syncthreads();
+                             });
 }
 
 // ---------------------------------------------------------------------------
 // phase: head = RMSNorm(src; g_final) -> unembedding -> online (max, argmax,
 // sum exp, second max) over the vocabulary, never writing logits (unless a
-// debug buffer is given). Each workgroup owns a contiguous row range and
-// writes one partial; the last workgroup merges the partials with a fixed
-// tree, takes the gate decision (readout) or the final token, and emits.
+// debug buffer is given). Each workgroup owns a contiguous row range split in
+// contiguous eighths, one per wave, streamed in blocks of kRS rows; the
+// workgroup writes one partial and the last workgroup merges the partials
+// with a fixed tree, takes the gate decision (readout) or the final token,
+// and emits.
 // ---------------------------------------------------------------------------
 struct Stat {
   float m;    // max logit
@@ -604,30 +790,43 @@ __device__ inline Stat stat_merge(Stat a, Stat b) {
   return w;
 }
 
-template <typename WT>
-__device__ void phase_head(const DevParams& p, int readout, int step, int wg, int nwg, float* xs,
-                           float* red, float* stl) {
-  rmsnorm_to_lds(readout ? p.z : p.h, p.g_final, p.H, p.eps, xs, red);
-  const WT* E = static_cast<const WT*>(p.embed);
-  float* dbg = readout ? p.dbg_logits_r : p.dbg_logits_f;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int nch = p.H / Elem<WT>::N;
-  const int rb = static_cast<int>(static_cast<int64_t>(p.V) * wg / nwg);
-  const int re = static_cast<int>(static_cast<int64_t>(p.V) * (wg + 1) / nwg);
-  constexpr int R = 4;
-  Stat st = stat_empty();
-  for (int r0 = rb + wave * R; r0 < re; r0 += kWaves * R) {
-    const int nv = min(R, re - r0);
-    float acc[R] = {0.f, 0.f, 0.f, 0.f};
-    rows_dot<WT, R>(E + static_cast<int64_t>(r0) * p.H, p.H, nv, xs, 0, nch, lane, acc);
-    wave_sum_n<R>(acc);
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-      if (r < nv) stat_push(st, acc[r], r0 + r);
-    if (dbg && lane == 0)
-      for (int r = 0; r < nv; ++r) dbg[r0 + r] = acc[r];
+__device__ __forceinline__ int head_row(const DevParams& p, int wg, int nwg, int wave) {
+  // workgroup wg owns rows [V wg / nwg, V (wg+1) / nwg); wave w the w-th eighth of them
+  const int64_t rb = static_cast<int64_t>(p.V) * wg / nwg;
+  const int64_t re = static_cast<int64_t>(p.V) * (wg + 1) / nwg;
+  return static_cast<int>(rb + (re - rb) * wave / kWaves);
+}
+
+template <typename WT, int CPL>
+struct HeadTask {
+  RowBlock<WT, kRS, CPL> a, b;
+  __device__ __forceinline__ static Tiling<WT, kRS, CPL> tiling(const DevParams& p, int wg, int nwg) {
+    return Tiling<WT, kRS, CPL>{head_row(p, wg, nwg, wave_id()), head_row(p, wg, nwg, wave_id() + 1), 0,
+                                p.H / Elem<WT>::N, 1};
   }
+  __device__ __forceinline__ void prefetch(const DevParams& p, int wg, int nwg) {
+    const auto tl = tiling(p, wg, nwg);
+    if (tl.count() > 0) tl.load(a, static_cast<const WT*>(p.embed), p.H, 0);
+  }
+};
+
+template <typename WT, int CPL>
+__device__ void phase_head(const DevParams& p, int readout, int step, int wg, int nwg, float* xs,
+                           float* red, HeadTask<WT, CPL>& t) {
+  rmsnorm_stage(readout ? p.z : p.h, p.g_final, p.H, p.eps, xs, red);
+  float* dbg = readout ? p.dbg_logits_r : p.dbg_logits_f;
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  Stat st = stat_empty();
+  stream_tiles<WT, kRS, CPL>(static_cast<const WT*>(p.embed), p.H, HeadTask<WT, CPL>::tiling(p, wg, nwg),
+                             xs, t.a, t.b, [&](int r0, int nr, const float(&acc)[kRS]) {
+#pragma unroll
+                              for (int r = 0; r < kRS; ++r)
+                                if (r < nr) stat_push(st, acc[r], r0 + r);
+                              if (dbg && lane == 0)
+                                for (int r = 0; r < nr; ++r) dbg[r0 + r] = acc[r];
+                            });
   __shared__ int last_flag;
+  float* stl = xs;  // the normalised vector is no longer needed: kWG * 4 floats
   __syncthreads();
   if (lane == 0) {
     stl[wave * 4 + 0] = st.m;
@@ -637,12 +836,12 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    Stat t = stat_empty();
+    Stat tt = stat_empty();
     for (int w = 0; w < kWaves; ++w)
-      t = stat_merge(t, Stat{stl[w * 4], stl[w * 4 + 1], stl[w * 4 + 2], __float_as_int(stl[w * 4 + 3])});
+      tt = stat_merge(tt, Stat{stl[w * 4], stl[w * 4 + 1], stl[w * 4 + 2], __float_as_int(stl[w * 4 + 3])});
     float* part = p.head_part + static_cast<int64_t>(wg) * 4;
-    st_coh2(part, t.m, t.s);
-    st_coh2(part + 2, t.m2, __int_as_float(t.idx));
+    st_coh2(part, tt.m, tt.s);
+    st_coh2(part + 2, tt.m2, __int_as_float(tt.idx));
     wait_stores();
     const uint32_t old = __hip_atomic_fetch_add(&p.counters->head[0], 1u, __ATOMIC_RELAXED,
                                                 __HIP_MEMORY_SCOPE_AGENT);
@@ -650,19 +849,22 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
   }
   __syncthreads();
   if (!last_flag) return;
-  Stat t = stat_empty();
+  Stat tt = stat_empty();
   for (int i = threadIdx.x; i < nwg; i += kWG) {
     const float* part = p.head_part + static_cast<int64_t>(i) * 4;
-    t = stat_merge(t, Stat{ld_coh(part), ld_coh(part + 1), ld_coh(part + 2),
-                           __float_as_int(ld_coh(part + 3))});
+    const uint64_t a = ld_coh_u64(part), b = ld_coh_u64(part + 2);
+    tt = stat_merge(tt, Stat{__uint_as_float(static_cast<uint32_t>(a)),
+                             __uint_as_float(static_cast<uint32_t>(a >> 32)),
+                             __uint_as_float(static_cast<uint32_t>(b)),
+                             static_cast<int>(static_cast<uint32_t>(b >> 32))});
   }
-  stl[threadIdx.x * 4 + 0] = t.m;
-  stl[threadIdx.x * 4 + 1] = t.s;
-  stl[threadIdx.x * 4 + 2] = t.m2;
-  stl[threadIdx.x * 4 + 3] = __int_as_float(t.idx);
+  stl[threadIdx.x * 4 + 0] = tt.m;
+  stl[threadIdx.x * 4 + 1] = tt.s;
+  stl[threadIdx.x * 4 + 2] = tt.m2;
+  stl[threadIdx.x * 4 + 3] = __int_as_float(tt.idx);
   __syncthreads();
   for (int stride = kWG / 2; stride > 0; stride >>= 1) {
-    if (threadIdx.x < stride) {
+    if (static_cast<int>(threadIdx.x) < stride) {
       const float* a = stl + threadIdx.x * 4;
       const float* b = stl + (threadIdx.x + stride) * 4;
       const Stat r = stat_merge(Stat{a[0], a[1], a[2], __float_as_int(a[3])},
@@ -715,70 +917,67 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
 // ---------------------------------------------------------------------------
 // phase: KV-absence fill after an exit. For every skipped layer l (exit_layer
 // .. L-1, 0-based): a = RMSNorm(h_exit; g_attn[l]); K_l[pos] = RoPE(W_k,l a),
-// V_l[pos] = W_v,l a. Items are layer-major groups of kWaves row pairs.
+// V_l[pos] = W_v,l a. Global wave gw owns row pairs gw, gw + W, ... over the
+// layers' k and v rows; the normalisation is staged once without gain and
+// each layer's gain is applied chunk by chunk.
 // ---------------------------------------------------------------------------
-template <typename WT>
+template <typename WT, int CPL>
 __device__ void phase_fill(const DevParams& p, int pos, int wg, int nwg, float* xs, float* red) {
-  const int nl = p.L - p.exit_layer;
-  const int KD = p.K * p.D;                 // row pairs per layer (k and v rows: 2*KD)
-  const int ipl = (KD + kWaves - 1) / kWaves;
-  const int items = nl * ipl;
-  if (wg >= items) return;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int KD = p.K * p.D;  // row pairs per layer (k and v rows: 2*KD)
+  const int total = (p.L - p.exit_layer) * KD;
+  if (wg * kWaves >= total) return;
+  rmsnorm_stage(p.h_exit, nullptr, p.H, p.eps, xs, red);
   const int nch = p.H / Elem<WT>::N;
-  const int AD = p.A * p.D;
-  int cur = -1;
-  for (int it = wg; it < items; it += nwg) {
-    const int l = p.exit_layer + it / ipl;
+  const int tw = nwg * kWaves;
+  RowBlock<WT, 2, CPL> blk;
+  for (int q = wg * kWaves + wave_id(); q < total; q += tw) {
+    const int l = p.exit_layer + q / KD;
+    const int r0 = p.A * p.D + 2 * (q - (q / KD) * KD);
     const LayerW lw = p.layers[l];
-    if (l != cur) {
-      rmsnorm_to_lds(p.h_exit, lw.g_attn, p.H, p.eps, xs, red);
-      cur = l;
-    }
-    const int pair = (it % ipl) * kWaves + wave;
-    if (pair >= KD) continue;
-    const int r0 = AD + 2 * pair;
-    float acc[2] = {0.f, 0.f};
-    rows_dot<WT, 2>(static_cast<const WT*>(lw.wqkv) + static_cast<int64_t>(r0) * p.H, p.H, 2, xs, 0,
-                    nch, lane, acc);
+    blk.load(static_cast<const WT*>(lw.wqkv), p.H, r0, 2, 0, nch);
+    float acc[2];
+    blk.dot_gain(xs, lw.g_attn, 2, 0, nch, acc);
     wave_sum_n<2>(acc);
-    if (lane == 0) store_qkv_pair<WT>(p, l, pos, r0, acc[0], acc[1]);
+    if ((threadIdx.x & 63) == 0) store_qkv_pair<WT>(p, l, pos, r0, acc[0], acc[1]);
   }
 }
 
 // readout: z = W_r h + b_r; workgroup 0 also keeps h as h_exit.
-template <typename WT>
-__device__ void phase_readout(const DevParams& p, int wg, int nwg, float* xs) {
-  if (wg == 0)
-    for (int i = threadIdx.x; i < p.H; i += kWG) st_coh(p.h_exit + i, ld_coh(p.h + i));
-  phase_gemv<WT, 2>(static_cast<const WT*>(p.ro_w), p.H, p.H, p.h, p.z, p.ro_b, 0, wg, nwg, xs);
+template <typename WT, int CPL>
+__device__ void phase_readout(const DevParams& p, int wg, int nwg, float* xs, RowTask<WT, CPL>& t) {
+  if (wg == 0) {
+    for (int i = threadIdx.x * 2; i < p.H; i += kWG * 2) {
+      const uint64_t v = ld_coh_u64(p.h + i);
+      st_coh_u64(p.h_exit + i, v);
+    }
+  }
+  phase_rows<WT, CPL>(static_cast<const WT*>(p.ro_w), p.H, p.H, p.h, p.z, p.ro_b, 0, wg, nwg, xs, t);
 }
 
 // ---------------------------------------------------------------------------
-// LDS layout: xs [vec] | red [64] | stat [kWG * 4]
+// LDS layout: xs [vec] | red [64] (block sums, per-wave partial rows)
 // ---------------------------------------------------------------------------
 __host__ __device__ inline int lds_vec_floats(const DevParams& p) {
   int v = p.H;
   if (p.F > v) v = p.F;
   if (p.A * p.D > v) v = p.A * p.D;
+  if (kWG * 4 > v) v = kWG * 4;
   const int am = attn_lds_floats(p.G, p.D);
   if (am > v) v = am;
   return (v + 63) & ~63;
 }
 
 size_t lds_bytes(const DevParams& p) {
-  return static_cast<size_t>(lds_vec_floats(p) + 64 + kWG * 4) * sizeof(float);
+  return static_cast<size_t>(lds_vec_floats(p) + 64) * sizeof(float);
 }
 
 struct Lds {
   float* xs;
   float* red;
-  float* stl;
 };
 
 __device__ inline Lds lds_carve(const DevParams& p, float* smem) {
-  const int v = lds_vec_floats(p);
-  return Lds{smem, smem + v, smem + v + 64};
+  return Lds{smem, smem + lds_vec_floats(p)};
 }
 
 // ---------------------------------------------------------------------------
@@ -788,56 +987,75 @@ enum OpKind : int {
   kOpQkv = 0, kOpAttn, kOpWo, kOpGateUp, kOpDown, kOpReadout, kOpHeadR, kOpHeadF, kOpFill
 };
 
-template <typename WT, int OP>
+template <typename WT, int CPL, int OP>
 __global__ __launch_bounds__(kWG) void k_op(DevParams p, int l, int pos, int step, int skip_if_exited) {
   extern __shared__ float smem[];
   if (skip_if_exited && ld_coh(&p.ctl->exited)) return;
   const Lds s = lds_carve(p, smem);
   const int wg = blockIdx.x, nwg = gridDim.x;
-  if constexpr (OP == kOpQkv) phase_qkv<WT>(p, l, pos, step, wg, nwg, s.xs, s.red);
+  if constexpr (OP == kOpQkv) {
+    QkvTask<WT, CPL> t;
+    t.prefetch(p, l, wg);
+    phase_qkv<WT, CPL>(p, l, pos, step, wg, nwg, s.xs, s.red, t);
+  }
   if constexpr (OP == kOpAttn) phase_attn<WT>(p, l, pos, wg, nwg, s.xs);
-  if constexpr (OP == kOpWo)
-    phase_gemv<WT, 2>(static_cast<const WT*>(p.layers[l].wo), p.H, p.A * p.D, p.o, p.h, nullptr, 1, wg,
-                      nwg, s.xs);
-  if constexpr (OP == kOpGateUp) phase_gateup<WT>(p, l, wg, nwg, s.xs, s.red);
-  if constexpr (OP == kOpDown)
-    phase_gemv_splitk<WT, 2>(static_cast<const WT*>(p.layers[l].wd), p.H, p.F, p.a, p.h, wg, nwg, s.xs,
-                             s.red);
-  if constexpr (OP == kOpReadout) phase_readout<WT>(p, wg, nwg, s.xs);
-  if constexpr (OP == kOpHeadR) phase_head<WT>(p, 1, step, wg, nwg, s.xs, s.red, s.stl);
-  if constexpr (OP == kOpHeadF) phase_head<WT>(p, 0, step, wg, nwg, s.xs, s.red, s.stl);
+  if constexpr (OP == kOpWo) {
+    const WT* W = static_cast<const WT*>(p.layers[l].wo);
+    RowTask<WT, CPL> t;
+    t.prefetch(W, p.H, p.A * p.D, wg);
+    phase_rows<WT, CPL>(W, p.H, p.A * p.D, p.o, p.h, nullptr, 1, wg, nwg, s.xs, t);
+  }
+  if constexpr (OP == kOpGateUp) {
+    GateUpTask<WT, CPL> t;
+    t.prefetch(p, l, wg, nwg);
+    phase_gateup<WT, CPL>(p, l, wg, nwg, s.xs, s.red, t);
+  }
+  if constexpr (OP == kOpDown) {
+    DownTask<WT, CPL> t;
+    t.prefetch(p, l, wg, nwg);
+    phase_down<WT, CPL>(p, l, wg, nwg, s.xs, s.red, t);
+  }
+  if constexpr (OP == kOpReadout) {
+    RowTask<WT, CPL> t;
+    t.prefetch(static_cast<const WT*>(p.ro_w), p.H, p.H, wg);
+    phase_readout<WT, CPL>(p, wg, nwg, s.xs, t);
+  }
+  if constexpr (OP == kOpHeadR || OP == kOpHeadF) {
+    HeadTask<WT, CPL> t;
+    t.prefetch(p, wg, nwg);
+    phase_head<WT, CPL>(p, OP == kOpHeadR, step, wg, nwg, s.xs, s.red, t);
+  }
   if constexpr (OP == kOpFill)
-    if (ld_coh(&p.ctl->exited)) phase_fill<WT>(p, pos, wg, nwg, s.xs, s.red);
+    if (ld_coh(&p.ctl->exited)) phase_fill<WT, CPL>(p, pos, wg, nwg, s.xs, s.red);
 }
 
 static int op_grid(const DevParams& p, int op, int pos, int head_wgs) {
   switch (op) {
     case kOpQkv: return ((p.qkv_rows >> 1) + kWaves - 1) / kWaves;
-    case kOpAttn: return (p.K * ((pos + 1 + kAttnSplit - 1) / kAttnSplit) + kWaves - 1) / kWaves;
-    case kOpWo: return (p.H + kWaves * 2 - 1) / (kWaves * 2);
-    case kOpGateUp: return (p.F + 2 * kWaves - 1) / (2 * kWaves);
-    case kOpDown: return (p.H + 1) / 2;
-    case kOpReadout: return (p.H + kWaves * 2 - 1) / (kWaves * 2);
+    case kOpAttn: return p.K * ((pos + 1 + kAttnSplit - 1) / kAttnSplit);
+    case kOpWo:
+    case kOpReadout: return (p.H + kWaves - 1) / kWaves;
+    case kOpGateUp: return (p.F + kWaves * 4 - 1) / (kWaves * 4);
+    case kOpDown: return (p.H + 5) / 6;
     case kOpHeadR:
     case kOpHeadF: return head_wgs;
     case kOpFill: {
-      const int nl = p.L - p.exit_layer;
-      const int ipl = (p.K * p.D + kWaves - 1) / kWaves;
-      return nl * ipl > 0 ? nl * ipl : 1;
+      const int total = (p.L - p.exit_layer) * p.K * p.D;
+      return total > 0 ? (total + kWaves - 1) / kWaves : 1;
     }
   }
   return 1;
 }
 
-template <typename WT>
+template <typename WT, int CPL>
 static hipError_t op(const DevParams& p, int kind, int l, int pos, int step, int skip, int head_wgs,
                      hipStream_t s) {
   const int grid = op_grid(p, kind, pos, head_wgs);
   const size_t lds = lds_bytes(p);
   switch (kind) {
-#define EE_OP_CASE(K)                                                                        \
-  case K:                                                                                    \
-    hipLaunchKernelGGL((k_op<WT, K>), dim3(grid), dim3(kWG), lds, s, p, l, pos, step, skip); \
+#define EE_OP_CASE(K)                                                                             \
+  case K:                                                                                         \
+    hipLaunchKernelGGL((k_op<WT, CPL, K>), dim3(grid), dim3(kWG), lds, s, p, l, pos, step, skip); \
     break;
     EE_OP_CASE(kOpQkv)
     EE_OP_CASE(kOpAttn)
@@ -853,78 +1071,34 @@ static hipError_t op(const DevParams& p, int kind, int l, int pos, int step, int
   return hipGetLastError();
 }
 
-template <typename WT>
+template <typename WT, int CPL>
 static hipError_t layer_ops(const DevParams& p, int l, int pos, int step, int skip, int hw,
                             hipStream_t s) {
   hipError_t e;
-  if ((e = op<WT>(p, kOpQkv, l, pos, step, skip, hw, s)) != hipSuccess) return e;
-  if ((e = op<WT>(p, kOpAttn, l, pos, step, skip, hw, s)) != hipSuccess) return e;
-  if ((e = op<WT>(p, kOpWo, l, pos, step, skip, hw, s)) != hipSuccess) return e;
-  if ((e = op<WT>(p, kOpGateUp, l, pos, step, skip, hw, s)) != hipSuccess) return e;
-  return op<WT>(p, kOpDown, l, pos, step, skip, hw, s);
+  if ((e = op<WT, CPL>(p, kOpQkv, l, pos, step, skip, hw, s)) != hipSuccess) return e;
+  if ((e = op<WT, CPL>(p, kOpAttn, l, pos, step, skip, hw, s)) != hipSuccess) return e;
+  if ((e = op<WT, CPL>(p, kOpWo, l, pos, step, skip, hw, s)) != hipSuccess) return e;
+  if ((e = op<WT, CPL>(p, kOpGateUp, l, pos, step, skip, hw, s)) != hipSuccess) return e;
+  return op<WT, CPL>(p, kOpDown, l, pos, step, skip, hw, s);
 }
 
 // One decode step (or one prompt position when emit_head == 0) per op.
-template <typename WT>
+template <typename WT, int CPL>
 static hipError_t step_per_op(const DevParams& p, int pos, int step, int emit_head, int hw,
                               hipStream_t s) {
   hipError_t e;
   const int Le = p.exit_layer;
   for (int l = 0; l < Le; ++l)
-    if ((e = layer_ops<WT>(p, l, pos, step, 0, hw, s)) != hipSuccess) return e;
+    if ((e = layer_ops<WT, CPL>(p, l, pos, step, 0, hw, s)) != hipSuccess) return e;
   if (Le > 0) {
-    if ((e = op<WT>(p, kOpReadout, 0, pos, step, 0, hw, s)) != hipSuccess) return e;
-    if ((e = op<WT>(p, kOpHeadR, 0, pos, step, 0, hw, s)) != hipSuccess) return e;
-    if ((e = op<WT>(p, kOpFill, 0, pos, step, 0, hw, s)) != hipSuccess) return e;
+    if ((e = op<WT, CPL>(p, kOpReadout, 0, pos, step, 0, hw, s)) != hipSuccess) return e;
+    if ((e = op<WT, CPL>(p, kOpHeadR, 0, pos, step, 0, hw, s)) != hipSuccess) return e;
+    if ((e = op<WT, CPL>(p, kOpFill, 0, pos, step, 0, hw, s)) != hipSuccess) return e;
   }
   for (int l = Le; l < p.L; ++l)
-    if ((e = layer_ops<WT>(p, l, pos, step, Le > 0, hw, s)) != hipSuccess) return e;
-  if (emit_head) return op<WT>(p, kOpHeadF, 0, pos, step, Le > 0, hw, s);
+    if ((e = layer_ops<WT, CPL>(p, l, pos, step, Le > 0, hw, s)) != hipSuccess) return e;
+  if (emit_head) return op<WT, CPL>(p, kOpHeadF, 0, pos, step, Le > 0, hw, s);
   return hipSuccess;
-}
-
-hipError_t launch_decode_per_op(const DevParams& p, int wbf16, int pos0, int n, int head_wgs,
-                                hipStream_t s) {
-  for (int i = 0; i < n; ++i) {
-    const hipError_t e = wbf16 ? step_per_op<uint16_t>(p, pos0 + i, i, 1, head_wgs, s)
-                               : step_per_op<float>(p, pos0 + i, i, 1, head_wgs, s);
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
-}
-
-hipError_t launch_prefill_per_op(const DevParams& p, int wbf16, int pos0, const int32_t* d_tokens,
-                                 int n, int head_wgs, hipStream_t s) {
-  DevParams q = p;
-  q.exit_layer = 0;
-  q.force_tok = d_tokens;
-  q.force_exit = nullptr;
-  for (int i = 0; i < n; ++i) {
-    const int emit = (i == n - 1);
-    const hipError_t e = wbf16 ? step_per_op<uint16_t>(q, pos0 + i, i, emit, head_wgs, s)
-                               : step_per_op<float>(q, pos0 + i, i, emit, head_wgs, s);
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
-}
-
-__global__ __launch_bounds__(kWG) void k_copy_vec(float* dst, const float* src, int n) {
-  for (int i = blockIdx.x * kWG + threadIdx.x; i < n; i += gridDim.x * kWG) dst[i] = src[i];
-}
-
-hipError_t launch_head_eval(const DevParams& p, int wbf16, const float* d_x, int readout, int head_wgs,
-                            hipStream_t s) {
-  hipLaunchKernelGGL(k_copy_vec, dim3(8), dim3(kWG), 0, s, p.h, d_x, p.H);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  if (readout) {
-    e = wbf16 ? op<uint16_t>(p, kOpReadout, 0, 0, 0, 0, head_wgs, s)
-              : op<float>(p, kOpReadout, 0, 0, 0, 0, head_wgs, s);
-    if (e != hipSuccess) return e;
-  }
-  const int kind = readout ? kOpHeadR : kOpHeadF;
-  return wbf16 ? op<uint16_t>(p, kind, 0, 0, 0, 0, head_wgs, s)
-               : op<float>(p, kind, 0, 0, 0, 0, head_wgs, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -932,20 +1106,37 @@ hipError_t launch_head_eval(const DevParams& p, int wbf16, const float* d_x, int
 // ---------------------------------------------------------------------------
 constexpr uint64_t kWaitTicks = 400000000ull;  // ~4 s of the 100 MHz wall clock
 
-// All workgroups arrive, then wait for the count to reach target. The wait is
-// bounded: on time-out the abort flag is raised and every later wait returns
-// at once, so the grid always drains.
-__device__ inline void grid_barrier(const DevParams& p, uint32_t& target, int nwg) {
-  target += static_cast<uint32_t>(nwg);
+// Two-level grid barrier, split in arrive and wait so that a workgroup can
+// issue the next phase's weight loads in between. Epochs count barriers of
+// the launch; wait() for an epoch already reached returns at once. The wait
+// is bounded: on time-out the abort flag is raised and every later wait
+// returns at once, so the grid always drains.
+__device__ inline void bar_arrive(const DevParams& p, uint32_t& epoch, int wg, int nwg) {
+  ++epoch;
   wait_stores();
   __syncthreads();
   if (threadIdx.x == 0) {
-    uint32_t* ctr = &p.counters->barrier[0];
-    __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int g = wg & (kBarGroups - 1);
+    const uint32_t per = static_cast<uint32_t>((nwg - g + kBarGroups - 1) / kBarGroups);
+    const uint32_t old = __hip_atomic_fetch_add(&p.counters->group[g][0], 1u, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+    if (old == per * epoch - 1) {
+      const uint32_t ngroups = static_cast<uint32_t>(min(kBarGroups, nwg));
+      const uint32_t o2 = __hip_atomic_fetch_add(&p.counters->top[0], 1u, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
+      if (o2 == ngroups * epoch - 1)
+        __hip_atomic_store(&p.counters->gen[0], epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+__device__ inline void bar_wait(const DevParams& p, uint32_t epoch) {
+  if (threadIdx.x == 0) {
+    uint32_t* gen = &p.counters->gen[0];
     const uint64_t t0 = wall_clock64();
     while (true) {
-      const uint32_t v = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (static_cast<int32_t>(v - target) >= 0) break;
+      const uint32_t v = __hip_atomic_load(gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (static_cast<int32_t>(v - epoch) >= 0) break;
       if (__hip_atomic_load(&p.ctl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) break;
       if (wall_clock64() - t0 > kWaitTicks) {
         __hip_atomic_store(&p.ctl->abort, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -958,87 +1149,280 @@ __device__ inline void grid_barrier(const DevParams& p, uint32_t& target, int nw
   __syncthreads();
 }
 
-template <typename WT>
-__device__ void layer_persistent(const DevParams& p, int l, int pos, int step, int wg, int nwg,
-                                 const Lds& s, uint32_t& bt) {
-  phase_qkv<WT>(p, l, pos, step, wg, nwg, s.xs, s.red);
-  grid_barrier(p, bt, nwg);
-  phase_attn<WT>(p, l, pos, wg, nwg, s.xs);
-  grid_barrier(p, bt, nwg);
-  phase_gemv<WT, 2>(static_cast<const WT*>(p.layers[l].wo), p.H, p.A * p.D, p.o, p.h, nullptr, 1, wg,
-                    nwg, s.xs);
-  grid_barrier(p, bt, nwg);
-  phase_gateup<WT>(p, l, wg, nwg, s.xs, s.red);
-  grid_barrier(p, bt, nwg);
-  phase_gemv_splitk<WT, 2>(static_cast<const WT*>(p.layers[l].wd), p.H, p.F, p.a, p.h, wg, nwg, s.xs,
-                           s.red);
-  grid_barrier(p, bt, nwg);
+// The steps of the persistent program; each returns the updated barrier epoch.
+// Each reads the workgroup index through an opaque scalar move: values derived
+// from it (row ranges, weight pointers) are then computed inside the step
+// rather than hoisted out of the step and layer loops, where the invariants of
+// every phase would otherwise stay live together and exhaust the registers.
+__device__ __forceinline__ int opaque_wg() {
+  int v;
+  asm volatile("s_mov_b32 %0, %1" : "=s"(v) : "s"(static_cast<int>(blockIdx.x)));
+  return v;
+}
+#define EE_PHASE_FN template <typename WT, int CPL> __device__ __forceinline__ uint32_t
+
+EE_PHASE_FN run_qkv(const DevParams& p, int l, int pos, int step, float* smem, uint32_t ep) {
+  const int wg = opaque_wg();
+  const Lds s = lds_carve(p, smem);
+  QkvTask<WT, CPL> t;
+  t.prefetch(p, l, wg);
+  bar_wait(p, ep);
+  phase_qkv<WT, CPL>(p, l, pos, step, wg, gridDim.x, s.xs, s.red, t);
+  bar_arrive(p, ep, wg, gridDim.x);
+  return ep;
 }
 
-// prefill != 0: prompt positions, ungated, head only at the last position.
-template <typename WT>
-__global__ __launch_bounds__(kWG) void k_decode_persistent(DevParams p, int pos0, int n, int prefill) {
-  extern __shared__ float smem[];
+EE_PHASE_FN run_attn(const DevParams& p, int l, int pos, float* smem, uint32_t ep) {
+  const int wg = opaque_wg();
+  bar_wait(p, ep);
+  phase_attn<WT>(p, l, pos, wg, gridDim.x, smem);
+  bar_arrive(p, ep, wg, gridDim.x);
+  return ep;
+}
+
+EE_PHASE_FN run_wo(const DevParams& p, int l, float* smem, uint32_t ep) {
+  const int wg = opaque_wg();
   const Lds s = lds_carve(p, smem);
-  const int wg = blockIdx.x, nwg = gridDim.x;
-  uint32_t bt = 0;
+  const WT* W = static_cast<const WT*>(p.layers[l].wo);
+  RowTask<WT, CPL> t;
+  t.prefetch(W, p.H, p.A * p.D, wg);
+  bar_wait(p, ep);
+  phase_rows<WT, CPL>(W, p.H, p.A * p.D, p.o, p.h, nullptr, 1, wg, gridDim.x, s.xs, t);
+  bar_arrive(p, ep, wg, gridDim.x);
+  return ep;
+}
+
+EE_PHASE_FN run_gateup(const DevParams& p, int l, float* smem, uint32_t ep) {
+  const int wg = opaque_wg();
+  const Lds s = lds_carve(p, smem);
+  GateUpTask<WT, CPL> t;
+  t.prefetch(p, l, wg, gridDim.x);
+  bar_wait(p, ep);
+  phase_gateup<WT, CPL>(p, l, wg, gridDim.x, s.xs, s.red, t);
+  bar_arrive(p, ep, wg, gridDim.x);
+  return ep;
+}
+
+EE_PHASE_FN run_down(const DevParams& p, int l, float* smem, uint32_t ep) {
+  const int wg = opaque_wg();
+  const Lds s = lds_carve(p, smem);
+  DownTask<WT, CPL> t;
+  t.prefetch(p, l, wg, gridDim.x);
+  bar_wait(p, ep);
+  phase_down<WT, CPL>(p, l, wg, gridDim.x, s.xs, s.red, t);
+  bar_arrive(p, ep, wg, gridDim.x);
+  return ep;
+}
+
+EE_PHASE_FN run_readout(const DevParams& p, float* smem, uint32_t ep) {
+  const int wg = opaque_wg();
+  const Lds s = lds_carve(p, smem);
+  RowTask<WT, CPL> t;
+  t.prefetch(static_cast<const WT*>(p.ro_w), p.H, p.H, wg);
+  bar_wait(p, ep);
+  phase_readout<WT, CPL>(p, wg, gridDim.x, s.xs, t);
+  bar_arrive(p, ep, wg, gridDim.x);
+  return ep;
+}
+
+EE_PHASE_FN run_head(const DevParams& p, int readout, int step, float* smem, uint32_t ep) {
+  const int wg = opaque_wg();
+  const Lds s = lds_carve(p, smem);
+  HeadTask<WT, CPL> t;
+  t.prefetch(p, wg, gridDim.x);
+  bar_wait(p, ep);
+  phase_head<WT, CPL>(p, readout, step, wg, gridDim.x, s.xs, s.red, t);
+  bar_arrive(p, ep, wg, gridDim.x);
+  return ep;
+}
+
+EE_PHASE_FN run_fill(const DevParams& p, int pos, float* smem, uint32_t ep) {
+  const int wg = opaque_wg();
+  const Lds s = lds_carve(p, smem);
+  bar_wait(p, ep);
+  phase_fill<WT, CPL>(p, pos, wg, gridDim.x, s.xs, s.red);
+  bar_arrive(p, ep, wg, gridDim.x);
+  return ep;
+}
+#undef EE_PHASE_FN
+
+template <typename WT, int CPL>
+__device__ __forceinline__ uint32_t run_layer(const DevParams& p, int l, int pos, int step, float* smem,
+                                              uint32_t ep) {
+  ep = run_qkv<WT, CPL>(p, l, pos, step, smem, ep);
+  ep = run_attn<WT, CPL>(p, l, pos, smem, ep);
+  ep = run_wo<WT, CPL>(p, l, smem, ep);
+  ep = run_gateup<WT, CPL>(p, l, smem, ep);
+  return run_down<WT, CPL>(p, l, smem, ep);
+}
+
+// Parameters of the persistent kernel live in constant memory, one slot per
+// context: fields are read with scalar loads, and the kernel never copies the
+// parameter block into private memory (which a by-value argument of this size
+// in a kernel this large would cost).
+__constant__ DevParams c_params[kParamSlots];
+
+// prefill != 0: prompt positions, ungated, head only at the last position.
+// One loop over the layers (a single inlined copy of the layer code); the
+// readout and the gate run after layer exit_layer, and an exit leaves the
+// loop for the KV fill of the remaining layers.
+template <typename WT, int CPL>
+__global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_decode_persistent(
+    int slot, int pos0, int n, int prefill) {
+  extern __shared__ float smem[];
+  const DevParams& p = c_params[slot];
+  uint32_t ep = 0;
   const int Le = p.exit_layer;
   for (int i = 0; i < n; ++i) {
     if (__hip_atomic_load(&p.ctl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) break;
     const int pos = pos0 + i;
-    for (int l = 0; l < Le; ++l) layer_persistent<WT>(p, l, pos, i, wg, nwg, s, bt);
     int exited = 0;
-    if (Le > 0) {
-      phase_readout<WT>(p, wg, nwg, s.xs);
-      grid_barrier(p, bt, nwg);
-      phase_head<WT>(p, 1, i, wg, nwg, s.xs, s.red, s.stl);
-      grid_barrier(p, bt, nwg);
-      exited = ld_coh(&p.ctl->exited);
+    for (int l = 0; l < p.L; ++l) {
+      ep = run_layer<WT, CPL>(p, l, pos, i, smem, ep);
+      if (l + 1 == Le) {
+        ep = run_readout<WT, CPL>(p, smem, ep);
+        ep = run_head<WT, CPL>(p, 1, i, smem, ep);
+        bar_wait(p, ep);
+        exited = ld_coh(&p.ctl->exited);
+        if (exited) break;
+      }
     }
     if (exited) {
-      phase_fill<WT>(p, pos, wg, nwg, s.xs, s.red);
-      grid_barrier(p, bt, nwg);
-    } else {
-      for (int l = Le; l < p.L; ++l) layer_persistent<WT>(p, l, pos, i, wg, nwg, s, bt);
-      if (!prefill || i == n - 1) {
-        phase_head<WT>(p, 0, i, wg, nwg, s.xs, s.red, s.stl);
-        grid_barrier(p, bt, nwg);
-      }
+      if (Le < p.L) ep = run_fill<WT, CPL>(p, pos, smem, ep);
+    } else if (!prefill || i == n - 1) {
+      ep = run_head<WT, CPL>(p, 0, i, smem, ep);
     }
   }
 }
 
 __global__ void k_reset_barrier(Counters* c) {
-  if (threadIdx.x == 0) c->barrier[0] = 0u;
+  const int t = threadIdx.x;
+  if (t < kBarGroups) c->group[t][0] = 0u;
+  if (t == 0) {
+    c->top[0] = 0u;
+    c->gen[0] = 0u;
+  }
 }
 
-static hipError_t persistent(const DevParams& p, int wbf16, int pos0, int n, int prefill, int nwg,
-                             size_t lds, hipStream_t s) {
-  hipLaunchKernelGGL(k_reset_barrier, dim3(1), dim3(64), 0, s, p.counters);
+__global__ __launch_bounds__(kWG) void k_copy_vec(float* dst, const float* src, int n) {
+  for (int i = blockIdx.x * kWG + threadIdx.x; i < n; i += gridDim.x * kWG) dst[i] = src[i];
+}
+
+// ---------------------------------------------------------------------------
+// host dispatch over (storage type, chunks per lane)
+// ---------------------------------------------------------------------------
+int chunks_per_lane(const DevParams& p, int wbf16) {
+  const int nch = p.H / (wbf16 ? 8 : 4);
+  return (nch + 63) / 64;
+}
+
+template <typename F>
+static hipError_t dispatch(int wbf16, int cpl, F&& f) {
+  if (wbf16) {
+    switch (cpl) {
+      case 1: return f(uint16_t{}, std::integral_constant<int, 1>{});
+      case 2: return f(uint16_t{}, std::integral_constant<int, 2>{});
+      case 3: return f(uint16_t{}, std::integral_constant<int, 3>{});
+      case 4: return f(uint16_t{}, std::integral_constant<int, 4>{});
+    }
+  } else {
+    switch (cpl) {
+      case 1: return f(float{}, std::integral_constant<int, 1>{});
+      case 2: return f(float{}, std::integral_constant<int, 2>{});
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_decode_per_op(const DevParams& p, int wbf16, int pos0, int n, int head_wgs,
+                                hipStream_t s) {
+  return dispatch(wbf16, chunks_per_lane(p, wbf16), [&](auto wt, auto cpl) {
+    using WT = decltype(wt);
+    for (int i = 0; i < n; ++i) {
+      const hipError_t e = step_per_op<WT, decltype(cpl)::value>(p, pos0 + i, i, 1, head_wgs, s);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  });
+}
+
+hipError_t launch_prefill_per_op(const DevParams& p, int wbf16, int pos0, const int32_t* d_tokens,
+                                 int n, int head_wgs, hipStream_t s) {
+  DevParams q = p;
+  q.exit_layer = 0;
+  q.force_tok = d_tokens;
+  q.force_exit = nullptr;
+  return dispatch(wbf16, chunks_per_lane(p, wbf16), [&](auto wt, auto cpl) {
+    using WT = decltype(wt);
+    for (int i = 0; i < n; ++i) {
+      const hipError_t e =
+          step_per_op<WT, decltype(cpl)::value>(q, pos0 + i, i, i == n - 1, head_wgs, s);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  });
+}
+
+hipError_t launch_head_eval(const DevParams& p, int wbf16, const float* d_x, int readout, int head_wgs,
+                            hipStream_t s) {
+  hipLaunchKernelGGL(k_copy_vec, dim3(8), dim3(kWG), 0, s, p.h, d_x, p.H);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  DevParams pp = p;
-  void* args[] = {&pp, &pos0, &n, &prefill};
-  const void* fn = wbf16 ? reinterpret_cast<const void*>(&k_decode_persistent<uint16_t>)
-                         : reinterpret_cast<const void*>(&k_decode_persistent<float>);
-  return hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(kWG), args, static_cast<unsigned>(lds), s);
+  return dispatch(wbf16, chunks_per_lane(p, wbf16), [&](auto wt, auto cpl) {
+    using WT = decltype(wt);
+    constexpr int C = decltype(cpl)::value;
+    if (readout) {
+      const hipError_t e2 = op<WT, C>(p, kOpReadout, 0, 0, 0, 0, head_wgs, s);
+      if (e2 != hipSuccess) return e2;
+    }
+    return op<WT, C>(p, readout ? kOpHeadR : kOpHeadF, 0, 0, 0, 0, head_wgs, s);
+  });
 }
 
-hipError_t launch_decode_persistent(const DevParams& p, int wbf16, int pos0, int n, int nwg,
-                                    size_t lds, hipStream_t s) {
-  return persistent(p, wbf16, pos0, n, 0, nwg, lds, s);
+static const void* persistent_fn(int wbf16, int cpl) {
+  if (wbf16) {
+    switch (cpl) {
+      case 1: return reinterpret_cast<const void*>(&k_decode_persistent<uint16_t, 1>);
+      case 2: return reinterpret_cast<const void*>(&k_decode_persistent<uint16_t, 2>);
+      case 3: return reinterpret_cast<const void*>(&k_decode_persistent<uint16_t, 3>);
+      case 4: return reinterpret_cast<const void*>(&k_decode_persistent<uint16_t, 4>);
+    }
+  } else {
+    switch (cpl) {
+      case 1: return reinterpret_cast<const void*>(&k_decode_persistent<float, 1>);
+      case 2: return reinterpret_cast<const void*>(&k_decode_persistent<float, 2>);
+    }
+  }
+  return nullptr;
 }
 
-hipError_t launch_prefill_persistent(const DevParams& p, int wbf16, int pos0, int n, int nwg,
-                                     size_t lds, hipStream_t s) {
-  return persistent(p, wbf16, pos0, n, 1, nwg, lds, s);
+static hipError_t persistent(const PersistentLaunch& L, int pos0, int n, int prefill) {
+  const DevParams& p = *L.params_host;
+  const void* fn = persistent_fn(L.wbf16, chunks_per_lane(p, L.wbf16));
+  if (!fn || L.slot < 0 || L.slot >= kParamSlots) return hipErrorInvalidValue;
+  hipError_t e = hipMemcpyToSymbolAsync(HIP_SYMBOL(c_params), L.params_host, sizeof(DevParams),
+                                        sizeof(DevParams) * L.slot, hipMemcpyHostToDevice, L.stream);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_reset_barrier, dim3(1), dim3(64), 0, L.stream, p.counters);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  int slot = L.slot;
+  void* args[] = {&slot, &pos0, &n, &prefill};
+  return hipLaunchCooperativeKernel(fn, dim3(L.nwg), dim3(kWG), args, static_cast<unsigned>(L.lds),
+                                    L.stream);
 }
 
-int persistent_max_wgs_per_cu(int wbf16, size_t lds) {
+hipError_t launch_decode_persistent(const PersistentLaunch& L, int pos0, int n) {
+  return persistent(L, pos0, n, 0);
+}
+
+hipError_t launch_prefill_persistent(const PersistentLaunch& L, int pos0, int n) {
+  return persistent(L, pos0, n, 1);
+}
+
+int persistent_max_wgs_per_cu(const DevParams& p, int wbf16, size_t lds) {
   int nb = 0;
-  const void* fn = wbf16 ? reinterpret_cast<const void*>(&k_decode_persistent<uint16_t>)
-                         : reinterpret_cast<const void*>(&k_decode_persistent<float>);
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, kWG, lds) != hipSuccess) return 0;
+  const void* fn = persistent_fn(wbf16, chunks_per_lane(p, wbf16));
+  if (!fn || hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, kWG, lds) != hipSuccess) return 0;
   return nb;
 }
 
