@@ -190,9 +190,28 @@ int ee_head_eval(ee_ctx* ctx, int32_t readout_layer, const float* x,
  * Errors: EE_EINVAL (layer or pos out of range / not yet written). */
 int ee_read_kv(ee_ctx* ctx, int32_t layer, int32_t pos, float* k_out, float* v_out);
 
-/* Select the device program used for decoding: 1 = one persistent
- * cooperative kernel per call (default), 0 = one kernel per operation. */
-int ee_set_persistent(ee_ctx* ctx, int32_t on);
+/* Select the device program used for decoding and prefill: wgs_per_cu >= 1
+ * runs one persistent cooperative kernel per call with that many workgroups
+ * per compute unit (default 1); 0 runs one kernel per operation.
+ * Errors: EE_EINVAL (negative, or more workgroups than can be co-resident). */
+int ee_set_persistent(ee_ctx* ctx, int32_t wgs_per_cu);
+
+/* Run the persistent program with exactly nwg workgroups in total. Every
+ * phase distributes its work over any grid size, so results equal those of
+ * the default grid (up to the summation order of the head's exp-sums); a grid
+ * smaller than the number of compute units leaves units idle.
+ * Errors: EE_EINVAL (nwg < 1 or more than can be co-resident),
+ * EE_ESTATE (no persistent-kernel parameter slot). */
+int ee_set_persistent_grid(ee_ctx* ctx, int32_t nwg);
+
+/* Diagnostic timeline of the persistent kernel (test hook): with capacity > 0,
+ * later launches record the device wall clock (hipDeviceAttributeWallClockRate
+ * ticks) at each grid barrier of workgroup 0 — entry 2e when it arrives at
+ * barrier e (1-based within the launch), 2e+1 when its wait returns — up to
+ * capacity entries. capacity 0 turns it off. ee_read_timeline copies the
+ * first n entries of the latest launch into out (host). */
+int ee_set_timeline(ee_ctx* ctx, int32_t capacity);
+int ee_read_timeline(ee_ctx* ctx, uint64_t* out, int32_t n);
 
 /* Device time in milliseconds of the most recent ee_decode_n/_ex call's
  * kernels, measured with HIP events on the context's stream. */

@@ -75,7 +75,10 @@ def _load():
         "ee_head_eval": (C.c_int, [V, C.c_int32, _FP, _IP, _FP, _FP]),
         "ee_read_kv": (C.c_int, [V, C.c_int32, C.c_int32, _FP, _FP]),
         "ee_set_persistent": (C.c_int, [V, C.c_int32]),
+        "ee_set_persistent_grid": (C.c_int, [V, C.c_int32]),
         "ee_last_decode_ms": (C.c_int, [V, _FP]),
+        "ee_set_timeline": (C.c_int, [V, C.c_int32]),
+        "ee_read_timeline": (C.c_int, [V, C.POINTER(C.c_uint64), C.c_int32]),
         "ee_position": (C.c_int32, [V]),
         "ee_reset": (C.c_int, [V]),
         "ee_last_error": (C.c_char_p, [V]),
@@ -232,6 +235,20 @@ class Engine:
         """0/False: one kernel per operation; n >= 1 (True = 1): persistent kernel
         with n workgroups per compute unit."""
         self._check(lib.ee_set_persistent(self._ctx, int(wgs_per_cu)))
+
+    def ee_set_persistent_grid(self, nwg: int):
+        """Persistent kernel with exactly nwg workgroups."""
+        self._check(lib.ee_set_persistent_grid(self._ctx, int(nwg)))
+
+    def ee_set_timeline(self, capacity: int):
+        self._check(lib.ee_set_timeline(self._ctx, int(capacity)))
+        self._tl_cap = int(capacity)
+
+    def ee_read_timeline(self, n: int = None):
+        n = self._tl_cap if n is None else n
+        out = np.zeros(n, np.uint64)
+        self._check(lib.ee_read_timeline(self._ctx, out.ctypes.data_as(C.POINTER(C.c_uint64)), n))
+        return out
 
     def ee_last_decode_ms(self) -> float:
         ms = C.c_float()

@@ -72,6 +72,8 @@ struct ee_ctx {
   hipEvent_t ev0 = nullptr, ev1 = nullptr;
   float last_ms = 0.f;
   int slot = -1;                       // constant-memory parameter slot (persistent kernel)
+  uint64_t* d_timeline = nullptr;
+  int timeline_cap = 0;
   DevParams* params_pinned = nullptr;  // staging of the parameter block
   std::string err;
 };
@@ -150,6 +152,9 @@ int validate_config(const ee_config* g, std::string& why) {
   if ((g->head_dim * (g->wdtype == EE_BF16 ? 2 : 4)) % 128) {
     why = "a KV row (head_dim elements) must fill whole 128-byte lines"; return 0;
   }
+  if (g->head_dim * (g->wdtype == EE_BF16 ? 2 : 4) > 256) {
+    why = "a KV row (head_dim elements) must be at most 256 bytes"; return 0;
+  }
   if (g->vocab < 2) { why = "vocab must be >= 2"; return 0; }
   if (g->max_seq < 1) { why = "max_seq must be >= 1"; return 0; }
   if (!is_pow2(g->page_size)) { why = "page_size must be a power of two"; return 0; }
@@ -186,6 +191,8 @@ DevParams make_params(const ee_ctx* c, float tau, int exit_layer) {
   p.attn_part = c->d_attn_part; p.max_splits = c->max_splits;
   p.head_part = c->d_head_part; p.max_parts = c->max_parts;
   p.counters = c->d_counters; p.ctl = c->d_ctl;
+  p.timeline = c->d_timeline;
+  p.timeline_cap = c->timeline_cap;
   return p;
 }
 
@@ -801,6 +808,43 @@ int ee_set_persistent(ee_ctx* c, int32_t wgs_per_cu) {
   return EE_OK;
 }
 
+int ee_set_persistent_grid(ee_ctx* c, int32_t nwg) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  const int most = std::min(c->max_parts, c->n_cu * c->max_wgs_per_cu);
+  if (nwg < 1 || nwg > most)
+    return fail(c, EE_EINVAL, "persistent grid must hold 1.." + std::to_string(most) + " workgroups");
+  if (c->slot < 0) return fail(c, EE_ESTATE, "no free persistent-kernel parameter slot");
+  c->persistent = true;
+  c->nwg_persistent = nwg;
+  return EE_OK;
+}
+
+int ee_set_timeline(ee_ctx* c, int32_t capacity) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  if (capacity < 0) return fail(c, EE_EINVAL, "capacity must be >= 0");
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  dfree(c->d_timeline);
+  c->d_timeline = nullptr;
+  c->timeline_cap = 0;
+  if (capacity > 0) {
+    int r;
+    if ((r = dalloc(c, &c->d_timeline, sizeof(uint64_t) * capacity))) return r;
+    c->timeline_cap = capacity;
+  }
+  return EE_OK;
+}
+
+int ee_read_timeline(ee_ctx* c, uint64_t* out, int32_t n) {
+  if (!c || !out || n < 0) return EE_EINVAL;
+  c->err.clear();
+  if (n > c->timeline_cap) return fail(c, EE_EINVAL, "more entries requested than recorded");
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  HIPCHK(c, hipMemcpy(out, c->d_timeline, sizeof(uint64_t) * n, hipMemcpyDeviceToHost));
+  return EE_OK;
+}
+
 int ee_last_decode_ms(ee_ctx* c, float* out_ms) {
   if (!c || !out_ms) return EE_EINVAL;
   *out_ms = c->last_ms;
@@ -846,6 +890,7 @@ void ee_destroy(ee_ctx* c) {
   dfree(c->d_x); dfree(c->d_attn_part); dfree(c->d_head_part); dfree(c->d_counters); dfree(c->d_ctl);
   dfree(c->d_ring_tok); dfree(c->d_ring_exit); dfree(c->d_ring_would); dfree(c->d_ring_conf);
   dfree(c->d_force_tok); dfree(c->d_force_exit); dfree(c->d_dbg_r); dfree(c->d_dbg_f);
+  dfree(c->d_timeline);
   if (c->ev0) (void)hipEventDestroy(c->ev0);
   if (c->ev1) (void)hipEventDestroy(c->ev1);
   if (c->own_stream && c->stream) (void)hipStreamDestroy(c->stream);

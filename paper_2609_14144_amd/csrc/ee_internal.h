@@ -9,7 +9,8 @@ namespace ee {
 
 constexpr int kWG = 256;               // threads per workgroup, every kernel
 constexpr int kWaves = kWG / 64;       // 64-wide wavefronts per workgroup
-constexpr int kAttnSplit = kWaves * 64;  // positions per attention work item (64 per wave)
+constexpr int kPosPerWave = 16;             // attention positions per wave
+constexpr int kAttnSplit = kWaves * kPosPerWave;  // positions per attention work item
 constexpr int kMaxGroup = 8;           // max query heads per KV head
 constexpr int kMaxHeadDim = 256;
 constexpr int kBarGroups = 8;          // first level of the grid barrier (one per XCD)
@@ -106,6 +107,11 @@ struct DevParams {
   float* dbg_logits_r;
   float* dbg_logits_f;
   float* dbg_h_final;
+  // diagnostic timeline of the persistent kernel (may be null): workgroup 0
+  // records the wall clock at barrier epoch e: [2e] after arriving, [2e+1]
+  // when the wait returns
+  uint64_t* timeline;
+  int timeline_cap;  // entries
 };
 
 // Host launchers (defined in ee_kernels.hip).

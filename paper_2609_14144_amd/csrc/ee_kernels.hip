@@ -130,6 +130,20 @@ __device__ inline float wave_max(float v) {
   return v;
 }
 
+// Sum over aligned groups of 8 or 16 lanes (DPP within a row of 16 lanes);
+// every lane of a group gets the same value.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float group_sum(float v, bool sixteen) {
+  v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]: lane ^ 1
+  v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]: lane ^ 2
+  v += dpp<0x141>(v);  // row_half_mirror: the other quad of the 8
+  if (sixteen) v += dpp<0x140>(v);  // row_mirror: the other 8 of the 16
+  return v;
+}
+
 template <int R>
 __device__ inline void wave_sum_n(float (&v)[R]) {
 #pragma unroll
@@ -433,193 +447,366 @@ __device__ void phase_qkv(const DevParams& p, int l, int pos, int step, int wg, 
 // ---------------------------------------------------------------------------
 // phase: decode attention over positions 0..pos, grouped-query. Workgroup
 // item = (kv head, split of kAttnSplit positions); wave w of the item takes
-// 64 positions. Scores: lanes own positions (q of the G query heads sharing
-// the kv head broadcast from LDS). Weighted V: groups of D/N lanes read one
-// position's row in 16-byte chunks. The waves merge in LDS; with one split
-// the item writes o directly, otherwise it writes a partial (max, sum of exp,
-// weighted V) and the last split of the kv head merges in index order.
+// kPosPerWave positions. Lane (sub, dl) of a wave holds 16-byte chunk dl of
+// K and V rows sub + PPW k (LPP lanes per row, PPW rows per load, RPL rows
+// per lane): a row's dot product with q is summed over its LPP lanes with
+// DPP, the softmax statistics over the wave's rows stay in registers, and
+// the weighted V rows are summed over the PPW row groups. The waves merge in
+// LDS; with one split the item writes o directly, otherwise it writes a
+// partial (max, sum of exp, weighted V) and the last split of the kv head to
+// finish merges all splits in index order from LDS.
+//
+// Latency: every K and V row of a lane is loaded with independent loads. The
+// rows of positions before pos were written in earlier steps, so the
+// workgroup issues them (and the page-table lookups) before it waits on the
+// barrier that ends the projection phase; only the row of position pos,
+// written by that phase, is loaded after it.
 // ---------------------------------------------------------------------------
 __host__ __device__ inline int attn_wave_floats(int G, int D) {
-  return 2 * 64 + G * 64 + G * D + 2 * G;  // offsets | exp(score) | weighted V | m, l
+  return 2 * kPosPerWave + G * D + 2 * G;  // offsets | weighted V | m, l
 }
 __host__ __device__ inline int attn_lds_floats(int G, int D) {
   return G * D + kWaves * attn_wave_floats(G, D);
 }
 
+// ---------------------------------------------------------------------------
+// LDS layout: xs [vec] | red [64] (block sums, per-wave partial rows)
+// ---------------------------------------------------------------------------
+__host__ __device__ inline int lds_vec_floats(const DevParams& p) {
+  int v = p.H;
+  if (p.F > v) v = p.F;
+  if (p.A * p.D > v) v = p.A * p.D;
+  if (kWG * 4 > v) v = kWG * 4;
+  const int am = attn_lds_floats(p.G, p.D);
+  if (am > v) v = am;
+  return (v + 63) & ~63;
+}
+
+// Hides x from loop-invariant code motion: a value passed through here at the
+// top of a loop body is unpacked inside the loop instead of being unpacked
+// once into many more registers than the packed form takes.
+__device__ __forceinline__ void keep_packed(uint4& x) {
+  asm volatile("" : "+v"(x.x), "+v"(x.y), "+v"(x.z), "+v"(x.w));
+}
+
+// reductions over the PPW row groups of a wave (one value per group, read
+// from the group's first lane); every lane gets the same result
+template <int LPP>
+__device__ __forceinline__ float groups_max(float v) {
+  float m = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+#pragma unroll
+  for (int r = 1; r < 64 / LPP; ++r)
+    m = fmaxf(m, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), r * LPP)));
+  return m;
+}
+template <int LPP>
+__device__ __forceinline__ float groups_sum(float v) {
+  float s = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+#pragma unroll
+  for (int r = 1; r < 64 / LPP; ++r)
+    s += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), r * LPP));
+  return s;
+}
+
+// 16-byte chunks per cache row: 16 (256-byte rows) or 8 (128-byte rows)
 template <typename WT>
-__device__ void phase_attn(const DevParams& p, int l, int pos, int wg, int nwg, float* lds) {
+__device__ __forceinline__ int attn_row_chunks(const DevParams& p) {
+  return p.D / Elem<WT>::N;
+}
+
+// The K and V rows of one wave in registers; rows [0, nold) are positions
+// before pos, and when has_new, row nold is position pos.
+template <typename WT>
+struct AttnTask {
+  static constexpr int N = Elem<WT>::N;
+  static constexpr int kRowsMax = kPosPerWave * 16 / 64;  // rows per lane at LPP = 16
+  uint4 kr[kRowsMax], vr[kRowsMax];
+  uint4 knew, vnew;  // row nold, in the lanes of row group nold % PPW
+  int nold;
+  bool has_new;
+
+  __device__ __forceinline__ static int64_t* offw(const DevParams& p, float* lds) {
+    return reinterpret_cast<int64_t*>(lds + p.G * p.D + wave_id() * attn_wave_floats(p.G, p.D));
+  }
+  // cache offsets of the wave's positions (up to pos) of item it, into LDS
+  __device__ __forceinline__ void offsets(const DevParams& p, int l, int pos, int it, int nsplit,
+                                          float* lds) {
+    const int lane = threadIdx.x & 63;
+    const int kvh = it / nsplit, sp = it - kvh * nsplit;
+    const int ws0 = sp * kAttnSplit + wave_id() * kPosPerWave;
+    if (lane < kPosPerWave && ws0 + lane <= pos) offw(p, lds)[lane] = kv_offset(p, l, ws0 + lane, kvh);
+    __builtin_amdgcn_wave_barrier();
+  }
+  // Rows [0, n) into kr/vr. Slots of rows >= n load row n - 1 again (no
+  // per-lane branches; their weight is zero), so every slot holds finite data.
+  template <int LPP>
+  __device__ __forceinline__ void load_old(const DevParams& p, const int64_t* ow, int n) {
+    if (n <= 0) return;
+    constexpr int PPW = 64 / LPP, RPL = kPosPerWave / PPW;
+    const int lane = threadIdx.x & 63;
+    const int sub = lane / LPP, dl = lane - sub * LPP;
+    const WT* kp = static_cast<const WT*>(p.kpool);
+    const WT* vp = static_cast<const WT*>(p.vpool);
+#pragma unroll
+    for (int k = 0; k < RPL; ++k) {
+      const int64_t o = ow[min(sub + PPW * k, n - 1)] + dl * N;
+      kr[k] = *reinterpret_cast<const uint4*>(kp + o);
+      vr[k] = *reinterpret_cast<const uint4*>(vp + o);
+    }
+  }
+  __device__ __forceinline__ void clear() {
+#pragma unroll
+    for (int k = 0; k < kRowsMax; ++k) kr[k] = vr[k] = make_uint4(0u, 0u, 0u, 0u);
+    knew = vnew = make_uint4(0u, 0u, 0u, 0u);
+    nold = 0;
+    has_new = false;
+  }
+  // Before the barrier: offsets and the rows of positions < pos of the
+  // workgroup's first item.
+  template <int LPP>
+  __device__ __forceinline__ void prefetch(const DevParams& p, int l, int pos, int wg, float* lds) {
+    clear();
+    const int nsplit = (pos + kAttnSplit) / kAttnSplit;
+    if (wg >= p.K * nsplit) return;
+    const int ws0 = (wg % nsplit) * kAttnSplit + wave_id() * kPosPerWave;
+    offsets(p, l, pos, wg, nsplit, lds);
+    nold = max(0, min(kPosPerWave, pos - ws0));
+    has_new = pos >= ws0 && pos < ws0 + kPosPerWave;
+    load_old<LPP>(p, offw(p, lds), nold);
+  }
+  // After the barrier: the row of position pos (first item only).
+  template <int LPP>
+  __device__ __forceinline__ void load_new(const DevParams& p, float* lds) {
+    if (!has_new) return;
+    constexpr int PPW = 64 / LPP;
+    const int lane = threadIdx.x & 63;
+    const int sub = lane / LPP, dl = lane - sub * LPP;
+    if (sub == nold % PPW) {
+      const int64_t o = offw(p, lds)[nold] + dl * N;
+      knew = *reinterpret_cast<const uint4*>(static_cast<const WT*>(p.kpool) + o);
+      vnew = *reinterpret_cast<const uint4*>(static_cast<const WT*>(p.vpool) + o);
+    }
+  }
+  // the packed chunk of row slot k of this lane (the new row replaces the
+  // slot it falls in); a select of values, never a store to a computed slot
+  template <int LPP>
+  __device__ __forceinline__ uint4 krow(int k, int sub) const {
+    constexpr int PPW = 64 / LPP;
+    return (has_new && k == nold / PPW && sub == nold % PPW) ? knew : kr[k];
+  }
+  template <int LPP>
+  __device__ __forceinline__ uint4 vrow(int k, int sub) const {
+    constexpr int PPW = 64 / LPP;
+    return (has_new && k == nold / PPW && sub == nold % PPW) ? vnew : vr[k];
+  }
+};
+
+template <typename WT, int LPP>
+__device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, float* lds,
+                                          AttnTask<WT>& t) {
   constexpr int N = Elem<WT>::N;
+  constexpr int PPW = 64 / LPP, RPL = kPosPerWave / PPW;
   const int T = pos + 1;
   const int nsplit = (T + kAttnSplit - 1) / kAttnSplit;
-  const int items = p.K * nsplit;
-  if (wg >= items) return;
   const int G = p.G, D = p.D;
   const int PS = D + 2;
-  const int LPP = D / N, PPW = 64 / LPP;
   const int wave = wave_id(), lane = threadIdx.x & 63;
   const int sub = lane / LPP, dl = lane - sub * LPP;
-  float* qs = lds;  // [G][D] scaled q
+  float* qs = lds;  // [G][D] q (unscaled)
   float* wb = lds + G * D + wave * attn_wave_floats(G, D);
-  int64_t* offw = reinterpret_cast<int64_t*>(wb);  // [64]
-  float* pw = wb + 128;                            // [G][64]
-  float* accw = pw + G * 64;                       // [G][D]
-  float* mlw = accw + G * D;                       // [G] m, [G] l
-  const WT* kp = static_cast<const WT*>(p.kpool);
-  const WT* vp = static_cast<const WT*>(p.vpool);
+  float* accw = wb + 2 * kPosPerWave;  // [G][D]
+  float* mlw = accw + G * D;           // [G] m, [G] l
   __shared__ int last_flag;
 
-  for (int it = wg; it < items; it += nwg) {
-    const int kvh = it / nsplit, sp = it - kvh * nsplit;
-    const int ws0 = sp * kAttnSplit + wave * 64;
-    const int wn = max(0, min(64, T - ws0));  // positions of this wave
-    __syncthreads();
-    for (int i = threadIdx.x * 2; i < G * D; i += kWG * 2) {
-      const uint64_t v = ld_coh_u64(p.q + kvh * G * D + i);
-      qs[i] = __uint_as_float(static_cast<uint32_t>(v)) * p.attn_scale;
-      qs[i + 1] = __uint_as_float(static_cast<uint32_t>(v >> 32)) * p.attn_scale;
-    }
-    if (lane < wn) offw[lane] = kv_offset(p, l, ws0 + lane, kvh);
-    __syncthreads();
-    const bool valid = lane < wn;
-    float sc[kMaxGroup];
+  const int kvh = it / nsplit, sp = it - kvh * nsplit;
+  const int ws0 = sp * kAttnSplit + wave * kPosPerWave;
+  const int wn = max(0, min(kPosPerWave, T - ws0));  // positions of this wave
+  __syncthreads();
+  stage_coh(p.q + kvh * G * D, G * D, qs);
+  t.template load_new<LPP>(p, lds);
+  __syncthreads();
+
+  if (wn > 0) {
+    // Two query heads per pass. Loops over query heads stay rolled: the
+    // phase runs once per layer, and a fully unrolled body is bound by
+    // instruction fetch rather than arithmetic.
+#pragma nounroll
+    for (int g0 = 0; g0 < G; g0 += 2) {
+      const int g1 = min(g0 + 1, G - 1);
+      float qa[N], qb[N];
 #pragma unroll
-    for (int g = 0; g < kMaxGroup; ++g) sc[g] = 0.f;
-    if (valid) {
-      const uint4* kr = reinterpret_cast<const uint4*>(kp + offw[lane]);
-#pragma unroll 4
-      for (int c = 0; c < D / N; ++c) {
+      for (int e = 0; e < N; ++e) {
+        qa[e] = qs[g0 * D + dl * N + e];
+        qb[e] = qs[g1 * D + dl * N + e];
+      }
+      float sa[RPL], sb[RPL];
+      float ma = -INFINITY, mb = -INFINITY;
+#pragma unroll
+      for (int k = 0; k < RPL; ++k) {
+        uint4 kc = t.template krow<LPP>(k, sub);
+        keep_packed(kc);
         float kf[N];
-        Elem<WT>::unpack(kr[c], kf);
+        Elem<WT>::unpack(kc, kf);
+        float x = 0.f, y = 0.f;
 #pragma unroll
-        for (int g = 0; g < kMaxGroup; ++g) {
-          if (g < G) {
-            const float* qg = qs + g * D + c * N;
+        for (int e = 0; e < N; ++e) {
+          x = fmaf(qa[e], kf[e], x);
+          y = fmaf(qb[e], kf[e], y);
+        }
+        const bool valid = sub + PPW * k < wn;
+        sa[k] = valid ? group_sum(x, LPP == 16) * p.attn_scale : -INFINITY;
+        sb[k] = valid ? group_sum(y, LPP == 16) * p.attn_scale : -INFINITY;
+        ma = fmaxf(ma, sa[k]);
+        mb = fmaxf(mb, sb[k]);
+      }
+      ma = groups_max<LPP>(ma);
+      mb = groups_max<LPP>(mb);
+      float la = 0.f, lb = 0.f;
 #pragma unroll
-            for (int e = 0; e < N; ++e) sc[g] = fmaf(qg[e], kf[e], sc[g]);
-          }
+      for (int k = 0; k < RPL; ++k) {
+        sa[k] = expf(sa[k] - ma);  // exp(-inf) = 0 for rows past the wave's end
+        sb[k] = expf(sb[k] - mb);
+        la += sa[k];
+        lb += sb[k];
+      }
+      la = groups_sum<LPP>(la);
+      lb = groups_sum<LPP>(lb);
+      float aa[N], ab[N];
+#pragma unroll
+      for (int e = 0; e < N; ++e) aa[e] = ab[e] = 0.f;
+#pragma unroll
+      for (int k = 0; k < RPL; ++k) {
+        uint4 vc = t.template vrow<LPP>(k, sub);
+        keep_packed(vc);
+        float vf[N];
+        Elem<WT>::unpack(vc, vf);
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+          aa[e] = fmaf(sa[k], vf[e], aa[e]);
+          ab[e] = fmaf(sb[k], vf[e], ab[e]);
         }
       }
-    }
-    float mg[kMaxGroup], lg[kMaxGroup];
 #pragma unroll
-    for (int g = 0; g < kMaxGroup; ++g) {
-      mg[g] = -INFINITY;
-      lg[g] = 0.f;
-      if (g < G && wn > 0) {
-        const float v = valid ? sc[g] : -INFINITY;
-        const float m = wave_max(v);
-        const float e = valid ? expf(v - m) : 0.f;
-        mg[g] = m;
-        lg[g] = wave_sum(e);
-        pw[g * 64 + lane] = e;
+      for (int off = LPP; off < 64; off <<= 1) {
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+          aa[e] += __shfl_xor(aa[e], off, 64);
+          ab[e] += __shfl_xor(ab[e], off, 64);
+        }
       }
-    }
-    __syncthreads();
-    if (wn > 0) {
-      // query heads in groups of kVG to bound the accumulator registers
-      constexpr int kVG = 4;
-      for (int g0 = 0; g0 < G; g0 += kVG) {
-        float acc[kVG][N];
+      if (sub == 0) {
 #pragma unroll
-        for (int g = 0; g < kVG; ++g)
-#pragma unroll
-          for (int e = 0; e < N; ++e) acc[g][e] = 0.f;
-#pragma unroll 2
-        for (int j0 = 0; j0 < wn; j0 += PPW) {
-          const int j = j0 + sub;
-          if (j < wn) {
-            const uint4 vw = *reinterpret_cast<const uint4*>(vp + offw[j] + dl * N);
-            float vf[N];
-            Elem<WT>::unpack(vw, vf);
-#pragma unroll
-            for (int g = 0; g < kVG; ++g) {
-              if (g0 + g < G) {
-                const float pj = pw[(g0 + g) * 64 + j];
-#pragma unroll
-                for (int e = 0; e < N; ++e) acc[g][e] = fmaf(pj, vf[e], acc[g][e]);
-              }
-            }
-          }
-        }
-        for (int off = LPP; off < 64; off <<= 1) {
-#pragma unroll
-          for (int g = 0; g < kVG; ++g)
-#pragma unroll
-            for (int e = 0; e < N; ++e) acc[g][e] += __shfl_xor(acc[g][e], off, 64);
-        }
-        if (sub == 0) {
-#pragma unroll
-          for (int g = 0; g < kVG; ++g)
-            if (g0 + g < G)
-#pragma unroll
-              for (int e = 0; e < N; ++e) accw[(g0 + g) * D + dl * N + e] = acc[g][e];
+        for (int e = 0; e < N; ++e) {
+          accw[g0 * D + dl * N + e] = aa[e];
+          accw[g1 * D + dl * N + e] = ab[e];  // g1 == g0 writes the same value
         }
       }
       if (lane == 0) {
+        mlw[g0] = ma;
+        mlw[G + g0] = la;
+        mlw[g1] = mb;
+        mlw[G + g1] = lb;
+      }
+    }
+  }
+  __syncthreads();
+  // merge the waves of this item (fixed order)
+  const int nw = min(kWaves, (T - sp * kAttnSplit + kPosPerWave - 1) / kPosPerWave);
+  float* part = p.attn_part + (static_cast<int64_t>(kvh) * p.max_splits + sp) * G * PS;
+  const float* base0 = lds + G * D;
+  const int WF = attn_wave_floats(G, D);
+  for (int idx = threadIdx.x; idx < G * D; idx += kWG) {
+    const int g = idx / D;
+    float mw[kWaves], aw[kWaves], lw[kWaves];
 #pragma unroll
-        for (int g = 0; g < kMaxGroup; ++g) {
-          if (g < G) {
-            mlw[g] = mg[g];
-            mlw[G + g] = lg[g];
-          }
-        }
-      }
+    for (int w = 0; w < kWaves; ++w) {
+      const float* wb2 = base0 + w * WF + 2 * kPosPerWave;
+      mw[w] = w < nw ? wb2[G * D + g] : -INFINITY;
+      lw[w] = w < nw ? wb2[G * D + G + g] : 0.f;
+      aw[w] = w < nw ? wb2[idx] : 0.f;
     }
-    __syncthreads();
-    // merge the waves of this item (fixed order)
-    const int nw = min(kWaves, (T - sp * kAttnSplit + 63) / 64);
-    float* part = p.attn_part + (static_cast<int64_t>(kvh) * p.max_splits + sp) * G * PS;
-    const float* base0 = lds + G * D;
-    for (int idx = threadIdx.x; idx < G * D; idx += kWG) {
-      const int g = idx / D, d = idx - g * D;
-      float M = -INFINITY;
-      for (int w = 0; w < nw; ++w) {
-        const float* m = base0 + w * attn_wave_floats(G, D) + 128 + G * 64 + G * D;
-        M = fmaxf(M, m[g]);
-      }
-      float den = 0.f, num = 0.f;
-      for (int w = 0; w < nw; ++w) {
-        const float* wb2 = base0 + w * attn_wave_floats(G, D);
-        const float* ml = wb2 + 128 + G * 64 + G * D;
-        const float f = expf(ml[g] - M);
-        den = fmaf(f, ml[G + g], den);
-        num = fmaf(f, wb2[128 + G * 64 + g * D + d], num);
-      }
-      if (nsplit == 1) {
-        st_coh(p.o + (kvh * G + g) * D + d, num / den);
-      } else {
-        st_coh(part + g * PS + 2 + d, num);
-        if (d == 0) st_coh2(part + g * PS, M, den);
-      }
+    float M = mw[0];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) M = fmaxf(M, mw[w]);
+    float den = 0.f, num = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float f = w < nw ? expf(mw[w] - M) : 0.f;
+      den = fmaf(f, lw[w], den);
+      num = fmaf(f, aw[w], num);
     }
-    if (nsplit == 1) continue;
-    // the last split of this kv head to finish merges all splits into o
-    wait_stores();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      const uint32_t old = __hip_atomic_fetch_add(&p.counters->attn[kvh][0], 1u, __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_AGENT);
-      last_flag = (old == static_cast<uint32_t>(nsplit - 1));
+    if (nsplit == 1) {
+      st_coh(p.o + kvh * G * D + idx, num / den);
+    } else {
+      const int d = idx - g * D;
+      st_coh(part + g * PS + 2 + d, num);
+      if (d == 0) st_coh2(part + g * PS, M, den);
     }
-    __syncthreads();
-    if (!last_flag) continue;
-    const float* base = p.attn_part + static_cast<int64_t>(kvh) * p.max_splits * G * PS;
-    for (int idx = threadIdx.x; idx < G * D; idx += kWG) {
-      const int g = idx / D, d = idx - g * D;
-      float M = -INFINITY;
-      for (int s2 = 0; s2 < nsplit; ++s2) M = fmaxf(M, ld_coh(base + (s2 * G + g) * PS));
-      float den = 0.f, num = 0.f;
-#pragma unroll 4
-      for (int s2 = 0; s2 < nsplit; ++s2) {
-        const float* rec = base + (s2 * G + g) * PS;
-        const float f = expf(ld_coh(rec) - M);
-        den = fmaf(f, ld_coh(rec + 1), den);
-        num = fmaf(f, ld_coh(rec + 2 + d), num);
+  }
+  if (nsplit == 1) return;
+  // the last split of this kv head to finish merges all splits into o
+  wait_stores();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t old = __hip_atomic_fetch_add(&p.counters->attn[kvh][0], 1u, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+    last_flag = (old == static_cast<uint32_t>(nsplit - 1));
+  }
+  __syncthreads();
+  if (!last_flag) return;
+  // Splits are staged into LDS in chunks with batched loads; each thread
+  // keeps a running (max, denominator, numerator) per output element.
+  const float* base = p.attn_part + static_cast<int64_t>(kvh) * p.max_splits * G * PS;
+  const int rec = G * PS;
+  const int cap = lds_vec_floats(p) / rec;
+  for (int idx0 = 0; idx0 < G * D; idx0 += kWG) {
+    const int idx = idx0 + static_cast<int>(threadIdx.x);
+    const int g = min(idx, G * D - 1) / D, d = min(idx, G * D - 1) - g * D;
+    float Mx = -INFINITY, den = 0.f, num = 0.f;
+    for (int s0 = 0; s0 < nsplit; s0 += cap) {
+      const int ns = min(cap, nsplit - s0);
+      if (s0 > 0 || idx0 == 0 || nsplit > cap) {
+        if (s0 > 0 || idx0 > 0) __syncthreads();
+        stage_coh(base + static_cast<int64_t>(s0) * rec, ns * rec, lds);
+        __syncthreads();
       }
-      st_coh(p.o + (kvh * G + g) * D + d, num / den);
+      float m = Mx;
+      for (int s2 = 0; s2 < ns; ++s2) m = fmaxf(m, lds[s2 * rec + g * PS]);
+      const float f0 = expf(Mx - m);
+      den *= f0;
+      num *= f0;
+      for (int s2 = 0; s2 < ns; ++s2) {
+        const float* r = lds + s2 * rec + g * PS;
+        const float f = expf(r[0] - m);
+        den = fmaf(f, r[1], den);
+        num = fmaf(f, r[2 + d], num);
+      }
+      Mx = m;
     }
-    if (threadIdx.x == 0)
-      __hip_atomic_store(&p.counters->attn[kvh][0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (idx < G * D) st_coh(p.o + kvh * G * D + idx, num / den);
+  }
+  if (threadIdx.x == 0)
+    __hip_atomic_store(&p.counters->attn[kvh][0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The first item of the workgroup uses the rows t prefetched; further items
+// (more than one per workgroup only past nwg * kAttnSplit / K positions) load
+// all of theirs after the barrier.
+template <typename WT, int LPP>
+__device__ __forceinline__ void phase_attn(const DevParams& p, int l, int pos, int wg, int nwg,
+                                           float* lds, AttnTask<WT>& t) {
+  const int nsplit = (pos + kAttnSplit) / kAttnSplit;
+  const int items = p.K * nsplit;
+  for (int it = wg; it < items; it += nwg) {
+    if (it != wg) {
+      __syncthreads();  // offsets of the previous item may still be read
+      t.offsets(p, l, pos, it, nsplit, lds);
+      const int ws0 = (it % nsplit) * kAttnSplit + wave_id() * kPosPerWave;
+      t.nold = max(0, min(kPosPerWave, pos + 1 - ws0));
+      t.has_new = false;
+      t.template load_old<LPP>(p, AttnTask<WT>::offw(p, lds), t.nold);
+    }
+    attn_item<WT, LPP>(p, pos, it, lds, t);
   }
 }
 
@@ -797,12 +984,12 @@ __device__ __forceinline__ int head_row(const DevParams& p, int wg, int nwg, int
   return static_cast<int>(rb + (re - rb) * wave / kWaves);
 }
 
-template <typename WT, int CPL>
+template <typename WT, int CPL, int R = kRS>
 struct HeadTask {
-  RowBlock<WT, kRS, CPL> a, b;
-  __device__ __forceinline__ static Tiling<WT, kRS, CPL> tiling(const DevParams& p, int wg, int nwg) {
-    return Tiling<WT, kRS, CPL>{head_row(p, wg, nwg, wave_id()), head_row(p, wg, nwg, wave_id() + 1), 0,
-                                p.H / Elem<WT>::N, 1};
+  RowBlock<WT, R, CPL> a, b;
+  __device__ __forceinline__ static Tiling<WT, R, CPL> tiling(const DevParams& p, int wg, int nwg) {
+    return Tiling<WT, R, CPL>{head_row(p, wg, nwg, wave_id()), head_row(p, wg, nwg, wave_id() + 1), 0,
+                              p.H / Elem<WT>::N, 1};
   }
   __device__ __forceinline__ void prefetch(const DevParams& p, int wg, int nwg) {
     const auto tl = tiling(p, wg, nwg);
@@ -810,17 +997,17 @@ struct HeadTask {
   }
 };
 
-template <typename WT, int CPL>
+template <typename WT, int CPL, int R = kRS>
 __device__ void phase_head(const DevParams& p, int readout, int step, int wg, int nwg, float* xs,
-                           float* red, HeadTask<WT, CPL>& t) {
+                           float* red, HeadTask<WT, CPL, R>& t) {
   rmsnorm_stage(readout ? p.z : p.h, p.g_final, p.H, p.eps, xs, red);
   float* dbg = readout ? p.dbg_logits_r : p.dbg_logits_f;
   const int wave = wave_id(), lane = threadIdx.x & 63;
   Stat st = stat_empty();
-  stream_tiles<WT, kRS, CPL>(static_cast<const WT*>(p.embed), p.H, HeadTask<WT, CPL>::tiling(p, wg, nwg),
-                             xs, t.a, t.b, [&](int r0, int nr, const float(&acc)[kRS]) {
+  stream_tiles<WT, R, CPL>(static_cast<const WT*>(p.embed), p.H, HeadTask<WT, CPL, R>::tiling(p, wg, nwg),
+                           xs, t.a, t.b, [&](int r0, int nr, const float(&acc)[R]) {
 #pragma unroll
-                              for (int r = 0; r < kRS; ++r)
+                              for (int r = 0; r < R; ++r)
                                 if (r < nr) stat_push(st, acc[r], r0 + r);
                               if (dbg && lane == 0)
                                 for (int r = 0; r < nr; ++r) dbg[r0 + r] = acc[r];
@@ -954,19 +1141,6 @@ __device__ void phase_readout(const DevParams& p, int wg, int nwg, float* xs, Ro
   phase_rows<WT, CPL>(static_cast<const WT*>(p.ro_w), p.H, p.H, p.h, p.z, p.ro_b, 0, wg, nwg, xs, t);
 }
 
-// ---------------------------------------------------------------------------
-// LDS layout: xs [vec] | red [64] (block sums, per-wave partial rows)
-// ---------------------------------------------------------------------------
-__host__ __device__ inline int lds_vec_floats(const DevParams& p) {
-  int v = p.H;
-  if (p.F > v) v = p.F;
-  if (p.A * p.D > v) v = p.A * p.D;
-  if (kWG * 4 > v) v = kWG * 4;
-  const int am = attn_lds_floats(p.G, p.D);
-  if (am > v) v = am;
-  return (v + 63) & ~63;
-}
-
 size_t lds_bytes(const DevParams& p) {
   return static_cast<size_t>(lds_vec_floats(p) + 64) * sizeof(float);
 }
@@ -998,7 +1172,16 @@ __global__ __launch_bounds__(kWG) void k_op(DevParams p, int l, int pos, int ste
     t.prefetch(p, l, wg);
     phase_qkv<WT, CPL>(p, l, pos, step, wg, nwg, s.xs, s.red, t);
   }
-  if constexpr (OP == kOpAttn) phase_attn<WT>(p, l, pos, wg, nwg, s.xs);
+  if constexpr (OP == kOpAttn) {
+    AttnTask<WT> t;
+    if (attn_row_chunks<WT>(p) == 16) {
+      t.template prefetch<16>(p, l, pos, wg, s.xs);
+      phase_attn<WT, 16>(p, l, pos, wg, nwg, s.xs, t);
+    } else {
+      t.template prefetch<8>(p, l, pos, wg, s.xs);
+      phase_attn<WT, 8>(p, l, pos, wg, nwg, s.xs, t);
+    }
+  }
   if constexpr (OP == kOpWo) {
     const WT* W = static_cast<const WT*>(p.layers[l].wo);
     RowTask<WT, CPL> t;
@@ -1127,6 +1310,8 @@ __device__ inline void bar_arrive(const DevParams& p, uint32_t& epoch, int wg, i
       if (o2 == ngroups * epoch - 1)
         __hip_atomic_store(&p.counters->gen[0], epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+    if (p.timeline && wg == 0 && 2 * static_cast<int>(epoch) < p.timeline_cap)
+      p.timeline[2 * epoch] = wall_clock64();
   }
 }
 
@@ -1145,6 +1330,8 @@ __device__ inline void bar_wait(const DevParams& p, uint32_t epoch) {
       }
       __builtin_amdgcn_s_sleep(1);
     }
+    if (p.timeline && blockIdx.x == 0 && 2 * static_cast<int>(epoch) + 1 < p.timeline_cap)
+      p.timeline[2 * epoch + 1] = wall_clock64();
   }
   __syncthreads();
 }
@@ -1174,8 +1361,16 @@ EE_PHASE_FN run_qkv(const DevParams& p, int l, int pos, int step, float* smem, u
 
 EE_PHASE_FN run_attn(const DevParams& p, int l, int pos, float* smem, uint32_t ep) {
   const int wg = opaque_wg();
-  bar_wait(p, ep);
-  phase_attn<WT>(p, l, pos, wg, gridDim.x, smem);
+  AttnTask<WT> t;
+  if (attn_row_chunks<WT>(p) == 16) {
+    t.template prefetch<16>(p, l, pos, wg, smem);
+    bar_wait(p, ep);
+    phase_attn<WT, 16>(p, l, pos, wg, gridDim.x, smem, t);
+  } else {
+    t.template prefetch<8>(p, l, pos, wg, smem);
+    bar_wait(p, ep);
+    phase_attn<WT, 8>(p, l, pos, wg, gridDim.x, smem, t);
+  }
   bar_arrive(p, ep, wg, gridDim.x);
   return ep;
 }

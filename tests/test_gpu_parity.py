@@ -233,6 +233,38 @@ def test_persistent_and_per_op_agree_and_are_deterministic():
         assert abs(a["conf"] - b["conf"]) <= 1e-6
 
 
+def test_small_persistent_grids_cover_all_work():
+    """Persistent grids of 1 and 3 workgroups: every phase loops over several
+    items per workgroup (attention: 2 kv heads x 4 splits of a 1000-token
+    context). Rows and tokens match the default grid and the per-op program."""
+    name = "tiny_bf16"
+    cfg = synth.get_config(name)
+    P = 1000
+    prompt = synth.prompts(cfg, 12, P)
+    tau = tiny_tau(name)
+    runs = []
+    for grid in (None, 1, 3, 0):
+        e = engine(name, P + 8, grid != 0)
+        if grid:
+            e.ee_set_persistent_grid(grid)
+        g = e.ee_prefill(prompt)
+        d = [e.ee_decode_step_ex(tau, 2, force_exit=i % 2) for i in range(4)]
+        k, v = e.ee_read_kv(cfg.n_layers - 1, P + 2)
+        runs.append((g, d, k, v))
+    g0, d0, k0, v0 = runs[0]
+    for g, d, k, v in runs[1:]:
+        assert g == g0
+        np.testing.assert_array_equal(k, k0)
+        np.testing.assert_array_equal(v, v0)
+        for a, b in zip(d0, d):
+            assert a["token"] == b["token"] and a["exited"] == b["exited"]
+            np.testing.assert_array_equal(a["h_exit"], b["h_exit"])
+            np.testing.assert_array_equal(a["logits_readout"], b["logits_readout"])
+            assert abs(a["conf"] - b["conf"]) <= 1e-6
+    o = oracle_for(name, P + 8)
+    assert o.prefill(prompt) == g0 or o.last_prefill_stats[2] <= MARGIN
+
+
 @pytest.mark.parametrize("page_size", [1, 16, 64])
 def test_paging_ragged_prompts(page_size):
     name = "tiny_bf16"
