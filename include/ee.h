@@ -192,8 +192,9 @@ int ee_read_kv(ee_ctx* ctx, int32_t layer, int32_t pos, float* k_out, float* v_o
 
 /* Select the device program used for decoding and prefill: wgs_per_cu >= 1
  * runs one persistent cooperative kernel per call with that many workgroups
- * per compute unit (default 1); 0 runs one kernel per operation.
- * Errors: EE_EINVAL (negative, or more workgroups than can be co-resident). */
+ * per compute unit; a negative value selects as many as can be co-resident
+ * (the default); 0 runs one kernel per operation.
+ * Errors: EE_EINVAL (more workgroups than can be co-resident). */
 int ee_set_persistent(ee_ctx* ctx, int32_t wgs_per_cu);
 
 /* Run the persistent program with exactly nwg workgroups in total. Every

@@ -232,8 +232,11 @@ class Engine:
         return k, v
 
     def ee_set_persistent(self, wgs_per_cu):
-        """0/False: one kernel per operation; n >= 1 (True = 1): persistent kernel
-        with n workgroups per compute unit."""
+        """0/False: one kernel per operation; True (or a negative value): the
+        persistent kernel with as many workgroups per compute unit as can be
+        co-resident; n >= 2: n workgroups per compute unit."""
+        if wgs_per_cu is True:
+            wgs_per_cu = -1
         self._check(lib.ee_set_persistent(self._ctx, int(wgs_per_cu)))
 
     def ee_set_persistent_grid(self, nwg: int):

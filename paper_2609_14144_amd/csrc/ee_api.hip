@@ -573,7 +573,7 @@ int ee_create(const ee_config* cfg, void* hip_stream, ee_ctx** out) {
   if ((he = hipHostMalloc(reinterpret_cast<void**>(&c->params_pinned), sizeof(DevParams))) != hipSuccess)
     return bail(hip_fail(c, he, "hipHostMalloc parameter block"));
   // without a free parameter slot the context uses the one-kernel-per-operation program
-  c->nwg_persistent = (c->max_wgs_per_cu > 0 && c->slot >= 0) ? c->n_cu : 0;
+  c->nwg_persistent = (c->max_wgs_per_cu > 0 && c->slot >= 0) ? c->n_cu * c->max_wgs_per_cu : 0;
   c->persistent = c->nwg_persistent > 0;
   c->head_wgs = 2 * c->n_cu;
   c->max_parts = std::max(c->head_wgs, c->nwg_persistent);
@@ -794,11 +794,11 @@ int ee_read_kv(ee_ctx* c, int32_t layer, int32_t pos, float* k_out, float* v_out
 int ee_set_persistent(ee_ctx* c, int32_t wgs_per_cu) {
   if (!c) return EE_EINVAL;
   c->err.clear();
-  if (wgs_per_cu < 0) return fail(c, EE_EINVAL, "wgs_per_cu must be >= 0");
   if (wgs_per_cu == 0) {
     c->persistent = false;
     return EE_OK;
   }
+  if (wgs_per_cu < 0) wgs_per_cu = std::max(1, c->max_wgs_per_cu);
   if (wgs_per_cu > c->max_wgs_per_cu)
     return fail(c, EE_EINVAL, "at most " + std::to_string(c->max_wgs_per_cu) +
                                   " persistent workgroups per CU can be co-resident");

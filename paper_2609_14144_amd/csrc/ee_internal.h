@@ -90,7 +90,7 @@ struct DevParams {
   float* q;                     // [A*D]
   float* o;                     // [A*D]
   float* a;                     // [F]
-  float* attn_part;             // [K][max_splits][G][D + 2]
+  float* attn_part;             // [K][max_splits][G][D] weighted V, then [K][max_splits][G][2] (max, sum)
   int max_splits;
   float* head_part;             // [max_parts][4]
   int max_parts;

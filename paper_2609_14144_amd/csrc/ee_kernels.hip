@@ -118,24 +118,18 @@ __device__ __forceinline__ uint64_t ld_coh_u64(const void* p) {
 // ---------------------------------------------------------------------------
 // reductions
 // ---------------------------------------------------------------------------
-__device__ inline float wave_sum(float v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  return v;
-}
-
-__device__ inline float wave_max(float v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
-  return v;
-}
-
-// Sum over aligned groups of 8 or 16 lanes (DPP within a row of 16 lanes);
-// every lane of a group gets the same value.
+// Reductions over a wave use DPP within rows of 16 lanes (a few cycles per
+// step) and read the four row results with readlane, instead of a chain of
+// LDS-routed lane shuffles (a round trip through LDS per step). Every lane
+// gets the same, fixed-order result.
 template <int CTRL>
 __device__ __forceinline__ float dpp(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
 }
+__device__ __forceinline__ float readlane(float v, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+// sum over aligned groups of 8 or 16 lanes
 __device__ __forceinline__ float group_sum(float v, bool sixteen) {
   v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]: lane ^ 1
   v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]: lane ^ 2
@@ -143,14 +137,30 @@ __device__ __forceinline__ float group_sum(float v, bool sixteen) {
   if (sixteen) v += dpp<0x140>(v);  // row_mirror: the other 8 of the 16
   return v;
 }
+__device__ __forceinline__ float group_max16(float v) {
+  v = fmaxf(v, dpp<0xB1>(v));
+  v = fmaxf(v, dpp<0x4E>(v));
+  v = fmaxf(v, dpp<0x141>(v));
+  return fmaxf(v, dpp<0x140>(v));
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+  v = group_sum(v, true);
+  return (readlane(v, 0) + readlane(v, 16)) + (readlane(v, 32) + readlane(v, 48));
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+  v = group_max16(v);
+  return fmaxf(fmaxf(readlane(v, 0), readlane(v, 16)), fmaxf(readlane(v, 32), readlane(v, 48)));
+}
 
 template <int R>
-__device__ inline void wave_sum_n(float (&v)[R]) {
+__device__ __forceinline__ void wave_sum_n(float (&v)[R]) {
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
+  for (int r = 0; r < R; ++r) v[r] = group_sum(v[r], true);
 #pragma unroll
-    for (int r = 0; r < R; ++r) v[r] += __shfl_xor(v[r], off, 64);
-  }
+  for (int r = 0; r < R; ++r)
+    v[r] = (readlane(v[r], 0) + readlane(v[r], 16)) + (readlane(v[r], 32) + readlane(v[r], 48));
 }
 
 // Sum over the workgroup; every thread gets the total. Fixed order.
@@ -479,6 +489,8 @@ __host__ __device__ inline int lds_vec_floats(const DevParams& p) {
   if (kWG * 4 > v) v = kWG * 4;
   const int am = attn_lds_floats(p.G, p.D);
   if (am > v) v = am;
+  const int mt = 3 * p.max_splits * p.G + p.G;  // merge tables of the last split
+  if (mt > v) v = mt;
   return (v + 63) & ~63;
 }
 
@@ -609,7 +621,6 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
   const int T = pos + 1;
   const int nsplit = (T + kAttnSplit - 1) / kAttnSplit;
   const int G = p.G, D = p.D;
-  const int PS = D + 2;
   const int wave = wave_id(), lane = threadIdx.x & 63;
   const int sub = lane / LPP, dl = lane - sub * LPP;
   float* qs = lds;  // [G][D] q (unscaled)
@@ -712,7 +723,9 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
   __syncthreads();
   // merge the waves of this item (fixed order)
   const int nw = min(kWaves, (T - sp * kAttnSplit + kPosPerWave - 1) / kPosPerWave);
-  float* part = p.attn_part + (static_cast<int64_t>(kvh) * p.max_splits + sp) * G * PS;
+  const int64_t kvrec = static_cast<int64_t>(kvh) * p.max_splits;
+  float* pacc = p.attn_part;                                           // [K][S][G][D]
+  float* pml = p.attn_part + static_cast<int64_t>(p.K) * p.max_splits * G * D;  // [K][S][G][2]
   const float* base0 = lds + G * D;
   const int WF = attn_wave_floats(G, D);
   for (int idx = threadIdx.x; idx < G * D; idx += kWG) {
@@ -738,9 +751,8 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
     if (nsplit == 1) {
       st_coh(p.o + kvh * G * D + idx, num / den);
     } else {
-      const int d = idx - g * D;
-      st_coh(part + g * PS + 2 + d, num);
-      if (d == 0) st_coh2(part + g * PS, M, den);
+      st_coh(pacc + (kvrec + sp) * G * D + idx, num);
+      if (idx - g * D == 0) st_coh2(pml + ((kvrec + sp) * G + g) * 2, M, den);
     }
   }
   if (nsplit == 1) return;
@@ -754,36 +766,62 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
   }
   __syncthreads();
   if (!last_flag) return;
-  // Splits are staged into LDS in chunks with batched loads; each thread
-  // keeps a running (max, denominator, numerator) per output element.
-  const float* base = p.attn_part + static_cast<int64_t>(kvh) * p.max_splits * G * PS;
-  const int rec = G * PS;
-  const int cap = lds_vec_floats(p) / rec;
-  for (int idx0 = 0; idx0 < G * D; idx0 += kWG) {
-    const int idx = idx0 + static_cast<int>(threadIdx.x);
-    const int g = min(idx, G * D - 1) / D, d = min(idx, G * D - 1) - g * D;
-    float Mx = -INFINITY, den = 0.f, num = 0.f;
-    for (int s0 = 0; s0 < nsplit; s0 += cap) {
-      const int ns = min(cap, nsplit - s0);
-      if (s0 > 0 || idx0 == 0 || nsplit > cap) {
-        if (s0 > 0 || idx0 > 0) __syncthreads();
-        stage_coh(base + static_cast<int64_t>(s0) * rec, ns * rec, lds);
-        __syncthreads();
-      }
-      float m = Mx;
-      for (int s2 = 0; s2 < ns; ++s2) m = fmaxf(m, lds[s2 * rec + g * PS]);
-      const float f0 = expf(Mx - m);
-      den *= f0;
-      num *= f0;
-      for (int s2 = 0; s2 < ns; ++s2) {
-        const float* r = lds + s2 * rec + g * PS;
-        const float f = expf(r[0] - m);
-        den = fmaf(f, r[1], den);
-        num = fmaf(f, r[2 + d], num);
-      }
-      Mx = m;
+  // One round trip for up to kSC splits: each thread issues the loads of its
+  // output elements for a batch of splits, then the (max, sum) table of all
+  // splits is staged; the split weights exp(m_s - M) and 1 / sum are formed
+  // once per query head.
+  constexpr int kIdx = kMaxGroup * kMaxHeadDim / 2 / kWG;  // G D <= 1024 (rows <= 256 bytes)
+  constexpr int kSC = 16;
+  const float* accb = pacc + kvrec * G * D;
+  float* mll = lds;                  // [nsplit][G][2]
+  float* fl = lds + 2 * nsplit * G;  // [nsplit][G] split weights, then [G] 1 / sum
+  float num[kIdx], av[kIdx][kSC];
+#pragma unroll
+  for (int k = 0; k < kIdx; ++k) {
+    num[k] = 0.f;
+    const int idx = static_cast<int>(threadIdx.x) + k * kWG;
+#pragma unroll
+    for (int s = 0; s < kSC; ++s)
+      av[k][s] = (idx < G * D && s < nsplit) ? ld_coh(accb + s * G * D + idx) : 0.f;
+  }
+  stage_coh(pml + kvrec * G * 2, 2 * nsplit * G, mll);
+  __syncthreads();
+  if (static_cast<int>(threadIdx.x) < G) {
+    const int g = threadIdx.x;
+    float M = -INFINITY;
+    for (int s = 0; s < nsplit; ++s) M = fmaxf(M, mll[(s * G + g) * 2]);
+    float den = 0.f;
+    for (int s = 0; s < nsplit; ++s) {
+      const float f = expf(mll[(s * G + g) * 2] - M);
+      fl[s * G + g] = f;
+      den = fmaf(f, mll[(s * G + g) * 2 + 1], den);
     }
-    if (idx < G * D) st_coh(p.o + kvh * G * D + idx, num / den);
+    fl[nsplit * G + g] = 1.f / den;
+  }
+  __syncthreads();
+  for (int s0 = 0; s0 < nsplit; s0 += kSC) {
+    if (s0 > 0) {
+#pragma unroll
+      for (int k = 0; k < kIdx; ++k) {
+        const int idx = static_cast<int>(threadIdx.x) + k * kWG;
+#pragma unroll
+        for (int s = 0; s < kSC; ++s)
+          av[k][s] = (idx < G * D && s0 + s < nsplit) ? ld_coh(accb + (s0 + s) * G * D + idx) : 0.f;
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kIdx; ++k) {
+      const int idx = min(static_cast<int>(threadIdx.x) + k * kWG, G * D - 1);
+      const int g = idx / D;
+#pragma unroll
+      for (int s = 0; s < kSC; ++s)
+        if (s0 + s < nsplit) num[k] = fmaf(fl[(s0 + s) * G + g], av[k][s], num[k]);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < kIdx; ++k) {
+    const int idx = static_cast<int>(threadIdx.x) + k * kWG;
+    if (idx < G * D) st_coh(p.o + kvh * G * D + idx, num[k] * fl[nsplit * G + idx / D]);
   }
   if (threadIdx.x == 0)
     __hip_atomic_store(&p.counters->attn[kvh][0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1462,7 +1500,7 @@ __constant__ DevParams c_params[kParamSlots];
 // readout and the gate run after layer exit_layer, and an exit leaves the
 // loop for the KV fill of the remaining layers.
 template <typename WT, int CPL>
-__global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_decode_persistent(
+__global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_decode_persistent(
     int slot, int pos0, int n, int prefill) {
   extern __shared__ float smem[];
   const DevParams& p = c_params[slot];

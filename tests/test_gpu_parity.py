@@ -134,23 +134,26 @@ def test_kv_cache_contents_including_fill(name):
     e = engine(name, 64, page_size=16)
     e.ee_prefill(prompt)
     e.ee_decode_n_ex(0.5, 2, 8, force_tokens=toks, force_exit=fe)
-    bad = 0
-    total = 0
     for l in range(cfg.n_layers):
         for t in range(TINY_P + 8):
             k, v = e.ee_read_kv(l, t)
             for got, ref in ((k, o.kcache[l, t].reshape(-1)), (v, o.vcache[l, t].reshape(-1))):
                 err = np.abs(got - ref)
-                # fp32 accumulation over H terms: a few ulps of the vector's scale
-                tol = np.full(err.shape, 1e-5 * np.max(np.abs(ref)))
-                if cfg.wdtype == "bf16":
-                    # identical storage rounding: equal, or one bf16 step apart where
-                    # the fp32 value sat within accumulation noise of a midpoint
-                    tol = np.maximum(tol, np.abs(ref) * 2.0 ** -7 * 1.01)
-                    bad += int(np.sum(err > 0))
-                assert np.all(err <= tol + 1e-30), (l, t, float(err.max()))
-                total += got.size
-    assert bad <= max(4, total // 200), (bad, total)
+                scale = np.max(np.abs(ref))
+                if cfg.wdtype == "f32":
+                    # fp32 accumulation over H terms: a few ulps of the vector's scale
+                    assert np.all(err <= 1e-5 * scale), (l, t, float(err.max()))
+                    continue
+                # Both sides store the cache in bf16. Where an fp32 value sat within
+                # accumulation noise of a rounding midpoint the two round apart by one
+                # step of the element, and that difference in an earlier layer or
+                # position perturbs later entries by about one bf16 step of the
+                # vector's scale. A wrong position, layer, rotation or a missing fill
+                # is off by the order of the values themselves.
+                tol = (np.abs(ref) + scale) * 2.0 ** -7 * 1.01
+                assert np.all(err <= tol), (l, t, float(err.max()))
+                rms = np.sqrt(np.mean(err ** 2) / np.mean(ref ** 2))
+                assert rms <= 2.0 ** -8, (l, t, float(rms))
 
 
 def test_error_paths():
