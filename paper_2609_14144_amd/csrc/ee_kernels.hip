@@ -178,20 +178,21 @@ __device__ inline float block_sum(float v, float* red) {
 
 // ---------------------------------------------------------------------------
 // staging of activation vectors (written by other workgroups) into LDS:
-// coherent 8-byte loads, up to 8 per thread in flight. n is even.
+// coherent 8-byte loads, up to 24 per thread in flight. n is even.
 // ---------------------------------------------------------------------------
 __device__ inline void stage_coh(const float* x, int n, float* xs) {
   const int n2 = n >> 1;
   uint64_t* dst = reinterpret_cast<uint64_t*>(xs);
-  for (int base = 0; base < n2; base += 8 * kWG) {
-    uint64_t v[8];
+  constexpr int kB = 24;  // loads per thread in flight: 12288 floats per round trip
+  for (int base = 0; base < n2; base += kB * kWG) {
+    uint64_t v[kB];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < kB; ++k) {
       const int i = base + k * kWG + static_cast<int>(threadIdx.x);
       v[k] = i < n2 ? ld_coh_u64(x + 2 * i) : 0ull;
     }
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < kB; ++k) {
       const int i = base + k * kWG + static_cast<int>(threadIdx.x);
       if (i < n2) dst[i] = v[k];
     }
@@ -324,7 +325,7 @@ struct Tiling {
 template <typename WT, int R, int CPL, typename Emit>
 __device__ __forceinline__ void stream_tiles(const WT* W, int64_t ld, const Tiling<WT, R, CPL>& tl,
                                              const float* xs, RowBlock<WT, R, CPL>& a,
-                                             RowBlock<WT, R, CPL>& b, Emit&& emit) {
+                                             RowBlock<WT, R, CPL>& b, Emit&& emit, int preloaded = 1) {
   const int nt = tl.count();
   float tot[R];
 #pragma unroll
@@ -342,7 +343,7 @@ __device__ __forceinline__ void stream_tiles(const WT* W, int64_t ld, const Tili
     }
   };
   for (int t = 0; t < nt; t += 2) {
-    if (t + 1 < nt) tl.load(b, W, ld, t + 1);
+    if (t + 1 < nt && (t > 0 || preloaded < 2)) tl.load(b, W, ld, t + 1);
     consume(a, t);
     if (t + 1 >= nt) break;
     if (t + 2 < nt) tl.load(a, W, ld, t + 2);
@@ -771,7 +772,7 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
   // splits is staged; the split weights exp(m_s - M) and 1 / sum are formed
   // once per query head.
   constexpr int kIdx = kMaxGroup * kMaxHeadDim / 2 / kWG;  // G D <= 1024 (rows <= 256 bytes)
-  constexpr int kSC = 16;
+  constexpr int kSC = 8;
   const float* accb = pacc + kvrec * G * D;
   float* mll = lds;                  // [nsplit][G][2]
   float* fl = lds + 2 * nsplit * G;  // [nsplit][G] split weights, then [G] 1 / sum
@@ -886,7 +887,7 @@ __device__ void phase_rows(const WT* W, int rows, int cols, const float* x, floa
 // (2j = gate j, 2j+1 = up j). Global wave gw owns the contiguous output range
 // [gw F / W, (gw+1) F / W), streamed in blocks of two outputs.
 // ---------------------------------------------------------------------------
-constexpr int kRS = 2;  // rows per streamed block
+constexpr int kRS = 4;  // rows per streamed block
 
 __device__ __forceinline__ int gu_begin(const DevParams& p, int gw, int tw) {
   return static_cast<int>(static_cast<int64_t>(p.F) * gw / tw);
@@ -902,7 +903,9 @@ struct GateUpTask {
   }
   __device__ __forceinline__ void prefetch(const DevParams& p, int l, int wg, int nwg) {
     const auto tl = tiling(p, wg, nwg);
-    if (tl.count() > 0) tl.load(a, static_cast<const WT*>(p.layers[l].wgu), p.H, 0);
+    const WT* W = static_cast<const WT*>(p.layers[l].wgu);
+    if (tl.count() > 0) tl.load(a, W, p.H, 0);
+    if (tl.count() > 1) tl.load(b, W, p.H, 1);
   }
 };
 
@@ -924,7 +927,7 @@ __device__ void phase_gateup(const DevParams& p, int l, int wg, int nwg, float* 
                                 for (int i = 0; i < kRS / 2; ++i)
                                   if (2 * i < nr) st_coh(a_out + r0 / 2 + i, silu(acc[2 * i]) * acc[2 * i + 1]);
                               }
-                            });
+                            }, 2);
 }
 
 // ---------------------------------------------------------------------------
@@ -936,6 +939,7 @@ __device__ void phase_gateup(const DevParams& p, int l, int wg, int nwg, float* 
 template <typename WT, int CPL>
 struct DownTask {
   RowBlock<WT, kRS, CPL> a, b;
+  float hres;  // residual h[rb + threadIdx.x] of the workgroup's rows (first kWG rows)
   __device__ __forceinline__ static Tiling<WT, kRS, CPL> tiling(const DevParams& p, int wg, int nwg) {
     const int nch = p.F / Elem<WT>::N;
     const int longest = (nch + kWaves - 1) / kWaves;
@@ -944,9 +948,15 @@ struct DownTask {
                                 nch * wave_id() / kWaves, nch * (wave_id() + 1) / kWaves,
                                 max(1, (longest + 64 * CPL - 1) / (64 * CPL))};
   }
+  // Before the barrier: the first two tiles, and the residual rows (h is
+  // last written by the output projection, two barriers earlier).
   __device__ __forceinline__ void prefetch(const DevParams& p, int l, int wg, int nwg) {
     const auto tl = tiling(p, wg, nwg);
-    if (tl.count() > 0) tl.load(a, static_cast<const WT*>(p.layers[l].wd), p.F, 0);
+    const WT* W = static_cast<const WT*>(p.layers[l].wd);
+    if (tl.count() > 0) tl.load(a, W, p.F, 0);
+    if (tl.count() > 1) tl.load(b, W, p.F, 1);
+    const int r = tl.rb + static_cast<int>(threadIdx.x);
+    hres = r < tl.re ? ld_coh(p.h + r) : 0.f;
   }
 };
 
@@ -957,21 +967,28 @@ __device__ void phase_down(const DevParams& p, int l, int wg, int nwg, float* xs
   if (tl.rb >= tl.re) return;
   copy_stage(p.a, p.F, xs);
   const int wave = wave_id();
+  const int tid = threadIdx.x;
   float* h = p.h;
   stream_tiles<WT, kRS, CPL>(static_cast<const WT*>(p.layers[l].wd), p.F, tl, xs, t.a, t.b,
                              [&](int r0, int nr, const float(&acc)[kRS]) {
-                               if ((threadIdx.x & 63) == 0) {
+                               if ((tid & 63) == 0) {
 #pragma unroll
                                  for (int i = 0; i < kRS; ++i) red[wave * kRS + i] = acc[i];
                                }
                                __syncthreads();
-                               if (static_cast<int>(threadIdx.x) < nr) {
+                               // the thread that holds row r's residual updates it
+                               const int i = tid - (r0 - tl.rb);
+                               if (i >= 0 && i < nr) {
                                  float sum = 0.f;
-                                 for (int w = 0; w < kWaves; ++w) sum += red[w * kRS + threadIdx.x];
-                                 st_coh(h + r0 + threadIdx.x, ld_coh(h + r0 + threadIdx.x) + sum);
+                                 for (int w = 0; w < kWaves; ++w) sum += red[w * kRS + i];
+                                 st_coh(h + r0 + i, t.hres + sum);
+                               } else if (r0 - tl.rb + nr > kWG && tid < nr && r0 - tl.rb + tid >= kWG) {
+                                 float sum = 0.f;
+                                 for (int w = 0; w < kWaves; ++w) sum += red[w * kRS + tid];
+                                 st_coh(h + r0 + tid, ld_coh(h + r0 + tid) + sum);
                                }
                                __syncthreads();
-                             });
+                             }, 2);
 }
 
 // ---------------------------------------------------------------------------
@@ -1031,7 +1048,9 @@ struct HeadTask {
   }
   __device__ __forceinline__ void prefetch(const DevParams& p, int wg, int nwg) {
     const auto tl = tiling(p, wg, nwg);
-    if (tl.count() > 0) tl.load(a, static_cast<const WT*>(p.embed), p.H, 0);
+    const WT* W = static_cast<const WT*>(p.embed);
+    if (tl.count() > 0) tl.load(a, W, p.H, 0);
+    if (tl.count() > 1) tl.load(b, W, p.H, 1);
   }
 };
 
@@ -1049,7 +1068,7 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
                                 if (r < nr) stat_push(st, acc[r], r0 + r);
                               if (dbg && lane == 0)
                                 for (int r = 0; r < nr; ++r) dbg[r0 + r] = acc[r];
-                            });
+                            }, 2);
   __shared__ int last_flag;
   float* stl = xs;  // the normalised vector is no longer needed: kWG * 4 floats
   __syncthreads();
