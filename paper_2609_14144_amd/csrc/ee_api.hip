@@ -45,8 +45,11 @@ struct ee_ctx {
 
   float* d_cos = nullptr;
   float* d_sin = nullptr;
-  float *d_h = nullptr, *d_hexit = nullptr, *d_z = nullptr, *d_q = nullptr, *d_o = nullptr,
-        *d_a = nullptr;
+  // tagged activation words (value + producer tag), one block
+  uint64_t* d_tw = nullptr;
+  int64_t tw_words = 0;
+  uint64_t *d_h = nullptr, *d_hexit = nullptr, *d_z = nullptr, *d_q = nullptr, *d_o = nullptr,
+           *d_a = nullptr, *d_kvnew = nullptr, *d_dec = nullptr;
   float* d_attn_part = nullptr;
   int max_splits = 0;
   float* d_head_part = nullptr;
@@ -188,6 +191,7 @@ DevParams make_params(const ee_ctx* c, float tau, int exit_layer) {
   p.block_table = c->d_block_table;
   p.rope_cos = c->d_cos; p.rope_sin = c->d_sin;
   p.h = c->d_h; p.h_exit = c->d_hexit; p.z = c->d_z; p.q = c->d_q; p.o = c->d_o; p.a = c->d_a;
+  p.kvnew = c->d_kvnew; p.dec = c->d_dec; p.tw_all = c->d_tw; p.tw_words = c->tw_words;
   p.attn_part = c->d_attn_part; p.max_splits = c->max_splits;
   p.head_part = c->d_head_part; p.max_parts = c->max_parts;
   p.counters = c->d_counters; p.ctl = c->d_ctl;
@@ -302,11 +306,23 @@ int run_steps(ee_ctx* c, float tau, int exit_layer, int n, const int32_t* d_forc
   HIPCHK(c, hipMemcpy(&ctl, c->d_ctl, sizeof(ctl), hipMemcpyDeviceToHost));
   if (ctl.error != ee::kErrNone || ctl.abort) {
     c->have_next = false;
-    return fail(c, EE_EDEVICE, ctl.error == ee::kErrToken ? "device: token id out of range"
-                                                          : "device: bounded grid wait timed out");
+    return fail(c, EE_EDEVICE, ctl.error == ee::kErrToken  ? "device: token id out of range"
+                               : ctl.error == ee::kErrWait ? "device: bounded wait for a phase's input timed out"
+                                                           : "device: bounded grid wait timed out");
   }
   c->pos += n;
   c->have_next = true;
+  return EE_OK;
+}
+
+// fp32 values of n tagged device words into host memory
+int copy_untag(ee_ctx* c, float* dst, const uint64_t* src, size_t n) {
+  std::vector<uint64_t> w(n);
+  HIPCHK(c, hipMemcpy(w.data(), src, n * 8, hipMemcpyDeviceToHost));
+  for (size_t i = 0; i < n; ++i) {
+    const uint32_t b = static_cast<uint32_t>(w[i]);
+    memcpy(dst + i, &b, 4);
+  }
   return EE_OK;
 }
 
@@ -547,11 +563,21 @@ int ee_create(const ee_config* cfg, void* hip_stream, ee_ctx** out) {
         (he = hipMemcpy(c->d_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
       return bail(hip_fail(c, he, "hipMemcpy rope tables"));
   }
-  if ((r = dalloc(c, &c->d_h, H * 4)) || (r = dalloc(c, &c->d_hexit, H * 4)) ||
-      (r = dalloc(c, &c->d_z, H * 4)) || (r = dalloc(c, &c->d_q, A * D * 4)) ||
-      (r = dalloc(c, &c->d_o, A * D * 4)) || (r = dalloc(c, &c->d_a, F * 4)) ||
-      (r = dalloc(c, &c->d_x, H * 4)))
-    return bail(r);
+  {
+    const int64_t sizes[8] = {int64_t(H), int64_t(H), int64_t(H), int64_t(A * D), int64_t(A * D),
+                              int64_t(F), int64_t(2 * K * D), 8};
+    uint64_t** ptrs[8] = {&c->d_h, &c->d_hexit, &c->d_z, &c->d_q, &c->d_o, &c->d_a, &c->d_kvnew, &c->d_dec};
+    int64_t total = 0;
+    for (int i = 0; i < 8; ++i) total += (sizes[i] + 31) & ~int64_t(31);  // 256-byte aligned parts
+    if ((r = dalloc(c, &c->d_tw, total * 8)) || (r = dalloc(c, &c->d_x, H * 4))) return bail(r);
+    c->tw_words = total;
+    int64_t off = 0;
+    for (int i = 0; i < 8; ++i) {
+      *ptrs[i] = c->d_tw + off;
+      off += (sizes[i] + 31) & ~int64_t(31);
+    }
+    if ((he = hipMemset(c->d_tw, 0, total * 8)) != hipSuccess) return bail(hip_fail(c, he, "hipMemset"));
+  }
   c->max_splits = (g.max_seq + ee::kAttnSplit - 1) / ee::kAttnSplit;
   if ((r = dalloc(c, &c->d_attn_part, K * c->max_splits * (A / K) * (D + 2) * 4))) return bail(r);
   if ((r = dalloc(c, &c->d_counters, sizeof(ee::Counters)))) return bail(r);
@@ -657,9 +683,8 @@ int ee_decode_step_ex(ee_ctx* c, float tau, int32_t exit_layer, int32_t input_to
   dbg->readout_token = exit_layer > 0 ? ctl.readout_token : -1;
   dbg->full_token = ex ? -1 : ctl.full_token;
   dbg->conf_full = ex ? NAN : ctl.conf_full;
-  if (dbg->h_exit && exit_layer > 0)
-    HIPCHK(c, hipMemcpy(dbg->h_exit, c->d_hexit, H * 4, hipMemcpyDeviceToHost));
-  if (dbg->h_final && !ex) HIPCHK(c, hipMemcpy(dbg->h_final, c->d_h, H * 4, hipMemcpyDeviceToHost));
+  if (dbg->h_exit && exit_layer > 0 && (r = copy_untag(c, dbg->h_exit, c->d_hexit, H))) return r;
+  if (dbg->h_final && !ex && (r = copy_untag(c, dbg->h_final, c->d_h, H))) return r;
   if (dbg->logits_readout && exit_layer > 0)
     HIPCHK(c, hipMemcpy(dbg->logits_readout, c->d_dbg_r, V * 4, hipMemcpyDeviceToHost));
   if (dbg->logits_full && !ex)
@@ -886,7 +911,7 @@ void ee_destroy(ee_ctx* c) {
   dfree(c->d_layers); dfree(c->kpool); dfree(c->vpool); dfree(c->d_block_table);
   if (c->h_block_table) (void)hipHostFree(c->h_block_table);
   dfree(c->d_cos); dfree(c->d_sin);
-  dfree(c->d_h); dfree(c->d_hexit); dfree(c->d_z); dfree(c->d_q); dfree(c->d_o); dfree(c->d_a);
+  dfree(c->d_tw);
   dfree(c->d_x); dfree(c->d_attn_part); dfree(c->d_head_part); dfree(c->d_counters); dfree(c->d_ctl);
   dfree(c->d_ring_tok); dfree(c->d_ring_exit); dfree(c->d_ring_would); dfree(c->d_ring_conf);
   dfree(c->d_force_tok); dfree(c->d_force_exit); dfree(c->d_dbg_r); dfree(c->d_dbg_f);

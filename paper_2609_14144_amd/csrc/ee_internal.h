@@ -47,12 +47,15 @@ struct StepCtl {
   uint32_t pad[7];
 };
 
-enum : int32_t { kErrNone = 0, kErrBarrier = 1, kErrToken = 2 };
+enum : int32_t { kErrNone = 0, kErrBarrier = 1, kErrToken = 2, kErrWait = 3 };
 
 // Grid barrier / last-arriver counters. Each lives on its own 256-byte line.
 // Barrier: workgroup wg arrives on group[wg % 8]; the last arrival of a group
 // arrives on top; the last arrival on top publishes the barrier's epoch in
-// gen, which every workgroup polls.
+// gen, which every workgroup polls. attn/head count the arrivals of the
+// attention splits of a KV head and of the head workgroups; within one
+// persistent launch they only grow (the last arrival is recognised from the
+// number of arrivals expected so far), one kernel per operation resets them.
 struct Counters {
   uint32_t group[kBarGroups][64];
   uint32_t top[64];
@@ -83,13 +86,18 @@ struct DevParams {
   const int32_t* block_table;   // logical page -> physical page
   const float* rope_cos;        // [max_seq][D/2]
   const float* rope_sin;
-  // activations (fp32)
-  float* h;                     // [H] residual stream
-  float* h_exit;                // [H]
-  float* z;                     // [H] readout output
-  float* q;                     // [A*D]
-  float* o;                     // [A*D]
-  float* a;                     // [F]
+  // Activations passed between phases, as tagged words: low 32 bits the fp32
+  // value, high 32 bits the tag of the phase that wrote it (one 8-byte store).
+  uint64_t* h;                  // [H] residual stream
+  uint64_t* h_exit;             // [H] residual stream at the exit layer
+  uint64_t* z;                  // [H] readout output
+  uint64_t* q;                  // [A*D]
+  uint64_t* o;                  // [A*D]
+  uint64_t* a;                  // [F]
+  uint64_t* kvnew;              // [2*K*D] this step's K row, then V row (storage-rounded)
+  uint64_t* dec;                // [4] exited, token, readout confidence, gate decision
+  uint64_t* tw_all;             // all of the above, one block of tw_words words
+  int64_t tw_words;
   float* attn_part;             // [K][max_splits][G][D] weighted V, then [K][max_splits][G][2] (max, sum)
   int max_splits;
   float* head_part;             // [max_parts][4]
@@ -108,8 +116,8 @@ struct DevParams {
   float* dbg_logits_f;
   float* dbg_h_final;
   // diagnostic timeline of the persistent kernel (may be null): workgroup 0
-  // records the wall clock at barrier epoch e: [2e] after arriving, [2e+1]
-  // when the wait returns
+  // records the wall clock for phase e of the launch: [2e] when its inputs
+  // are in LDS, [2e+1] when it has issued its outputs
   uint64_t* timeline;
   int timeline_cap;  // entries
 };
@@ -133,6 +141,8 @@ hipError_t launch_prefill_per_op(const DevParams& p, int wbf16, int pos0, const 
 hipError_t launch_prefill_persistent(const PersistentLaunch& L, int pos0, int n);
 hipError_t launch_head_eval(const DevParams& p, int wbf16, const float* d_x, int readout,
                             int head_wgs, hipStream_t s);
+// copy the fp32 values of n tagged words to dst (device)
+hipError_t launch_untag(float* dst, const uint64_t* src, int n, hipStream_t s);
 size_t lds_bytes(const DevParams& p);
 int chunks_per_lane(const DevParams& p, int wbf16);
 int persistent_max_wgs_per_cu(const DevParams& p, int wbf16, size_t lds);

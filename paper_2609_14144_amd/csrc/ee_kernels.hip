@@ -3,8 +3,11 @@
 // Every operation of the step is a "phase": a device function that processes
 // work items wg, wg + nwg, ... of one operation. The same phases run either
 // as one kernel per operation (blockIdx.x = wg) or inside one persistent
-// cooperative kernel that runs whole decode steps, separated by grid barriers,
-// with the exit branch taken on the device.
+// cooperative kernel that runs whole decode steps with the exit branch taken
+// on the device. Inside the persistent kernel, phases hand activations to
+// each other as tagged words (value + tag of the producing phase): a consumer
+// polls its inputs until they carry the expected tag, so consecutive phases
+// need no grid barrier; one barrier ends every step and every KV fill.
 //
 // Numerics: weights bf16 (or fp32), activations and accumulation fp32, KV
 // cache entries stored in the weight type (round to nearest even for bf16).
@@ -24,8 +27,13 @@
 //     it in that launch, and every row starts on a 128-byte line of its own,
 //     so no L2 can hold a stale copy;
 //   * a producer waits for its own stores to complete (s_waitcnt vmcnt(0))
-//     before signalling with one relaxed atomic. No L2 writeback or
+//     before signalling with one relaxed atomic; a tagged word is its own
+//     signal (value and tag in one 8-byte store). No L2 writeback or
 //     invalidate is ever issued.
+//   * a buffer is rewritten only after every reader of its previous contents
+//     has produced something the writer itself waited for (the chain
+//     q -> o -> h -> a -> h runs through every workgroup that reads), or
+//     after a grid barrier (step ends, KV fill).
 #include <math.h>
 #include <stdint.h>
 
@@ -95,6 +103,14 @@ struct Elem<uint16_t> {  // bf16 bit patterns
   __device__ static inline void store_pair(uint16_t* p, float a, float b) {
     st_coh_u32(p, bits(a) | (bits(b) << 16));
   }
+  __device__ static inline float round(float x) { return __uint_as_float(bits(x) << 16); }
+  // N values that are exactly representable, back into a chunk
+  __device__ static inline uint4 pack(const float* f) {
+    return make_uint4((__float_as_uint(f[0]) >> 16) | (__float_as_uint(f[1]) & 0xffff0000u),
+                      (__float_as_uint(f[2]) >> 16) | (__float_as_uint(f[3]) & 0xffff0000u),
+                      (__float_as_uint(f[4]) >> 16) | (__float_as_uint(f[5]) & 0xffff0000u),
+                      (__float_as_uint(f[6]) >> 16) | (__float_as_uint(f[7]) & 0xffff0000u));
+  }
 };
 
 template <>
@@ -108,11 +124,123 @@ struct Elem<float> {
   }
   __device__ static inline float load(const float* p) { return *p; }
   __device__ static inline void store_pair(float* p, float a, float b) { st_coh2(p, a, b); }
+  __device__ static inline float round(float x) { return x; }
+  __device__ static inline uint4 pack(const float* f) {
+    return make_uint4(__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
+                      __float_as_uint(f[3]));
+  }
 };
 
 __device__ __forceinline__ uint64_t ld_coh_u64(const void* p) {
   return __hip_atomic_load(static_cast<uint64_t*>(const_cast<void*>(p)), __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
+}
+
+constexpr uint64_t kWaitTicks = 400000000ull;  // ~4 s of the 100 MHz wall clock
+
+// ---------------------------------------------------------------------------
+// tagged words. Sync describes a phase's inputs and outputs: with poll set
+// (persistent kernel), an input word is read until it carries its tag; the
+// wait is bounded, and on time-out the abort flag is raised so that every
+// later wait returns at once and the grid drains. Without poll (one kernel
+// per operation) inputs are complete when the kernel starts.
+// ---------------------------------------------------------------------------
+struct Sync {
+  bool poll;
+  uint32_t tin;    // tag of the main input
+  uint32_t tres;   // tag of the second input (residual, token, gate record)
+  uint32_t tout;   // tag of this phase's outputs
+  uint32_t cbase;  // arrivals on this phase's last-arriver counter before it (persistent)
+};
+
+__device__ __forceinline__ uint64_t tw_pack(float v, uint32_t tag) {
+  return (static_cast<uint64_t>(tag) << 32) | __float_as_uint(v);
+}
+__device__ __forceinline__ float tw_val(uint64_t w) { return __uint_as_float(static_cast<uint32_t>(w)); }
+__device__ __forceinline__ bool tw_ok(uint64_t w, uint32_t tag) { return static_cast<uint32_t>(w >> 32) == tag; }
+__device__ __forceinline__ void tw_store(uint64_t* p, float v, uint32_t tag) { st_coh_u64(p, tw_pack(v, tag)); }
+
+__device__ __forceinline__ bool aborted(const DevParams& p) {
+  return __hip_atomic_load(&p.ctl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
+}
+__device__ __noinline__ void raise_abort(const DevParams& p, int err) {
+  __hip_atomic_store(&p.ctl->abort, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  atomicMax(&p.ctl->error, err);
+}
+
+// one word, waited for
+__device__ inline uint64_t tw_wait(const DevParams& p, const uint64_t* w, uint32_t tag, bool poll) {
+  uint64_t v = ld_coh_u64(w);
+  if (!poll || tw_ok(v, tag)) return v;
+  const uint64_t t0 = wall_clock64();
+  while (true) {
+    __builtin_amdgcn_s_sleep(2);
+    v = ld_coh_u64(w);
+    if (tw_ok(v, tag) || aborted(p)) break;
+    if (wall_clock64() - t0 > kWaitTicks) {
+      raise_abort(p, kErrWait);
+      break;
+    }
+  }
+  return v;
+}
+
+// Polling loop shared by the readers below: the first pass loads every word;
+// later passes (after a short sleep) load again only the words that do not
+// carry the tag yet. Without poll, one pass.
+#define EE_TW_POLL(KB, ADDR, VALID)                                                 \
+  {                                                                               \
+    uint64_t t0_ = 0;                                                             \
+    for (int pass_ = 0;; ++pass_) {                                               \
+      _Pragma("unroll") for (int k = 0; k < (KB); ++k) {                          \
+        if ((VALID) && !tw_ok(v[k], tag)) v[k] = ld_coh_u64(ADDR);                \
+      }                                                                           \
+      if (!poll) break;                                                           \
+      bool ready_ = true;                                                         \
+      _Pragma("unroll") for (int k = 0; k < (KB); ++k) ready_ = ready_ && tw_ok(v[k], tag); \
+      if (ready_ || aborted(p)) break;                                            \
+      if (pass_ == 0) t0_ = wall_clock64();                                       \
+      else if (wall_clock64() - t0_ > kWaitTicks) {                               \
+        raise_abort(p, kErrWait);                                                 \
+        break;                                                                    \
+      }                                                                           \
+      __builtin_amdgcn_s_sleep(2);                                                \
+    }                                                                             \
+  }
+
+// M words from each of a and b (one lane's own words), waited for together
+template <int M>
+__device__ inline void tw_read2(const DevParams& p, const uint64_t* a, const uint64_t* b, uint32_t tag,
+                                bool poll, float* fa, float* fb) {
+  uint64_t v[2 * M];
+  const uint64_t none = tw_pack(0.f, tag + 1u);
+#pragma unroll
+  for (int k = 0; k < 2 * M; ++k) v[k] = none;
+  EE_TW_POLL(2 * M, (k < M ? a + k : b + (k - M)), true)
+#pragma unroll
+  for (int k = 0; k < M; ++k) {
+    fa[k] = tw_val(v[k]);
+    fb[k] = tw_val(v[M + k]);
+  }
+}
+
+// n words into xs[0..n) as floats, the whole workgroup; kB words per thread
+// are in flight at once. xs is complete after the caller's next barrier.
+template <int kB>
+__device__ inline void tw_stage(const DevParams& p, const uint64_t* src, int n, uint32_t tag, bool poll,
+                                float* xs) {
+  const uint64_t none = tw_pack(0.f, tag + 1u);
+  for (int base = 0; base < n; base += kB * kWG) {
+    uint64_t v[kB];
+#pragma unroll
+    for (int k = 0; k < kB; ++k) v[k] = base + k * kWG + static_cast<int>(threadIdx.x) < n ? none : tw_pack(0.f, tag);
+    EE_TW_POLL(kB, src + base + k * kWG + threadIdx.x, true)
+#pragma unroll
+    for (int k = 0; k < kB; ++k) {
+      const int i = base + k * kWG + static_cast<int>(threadIdx.x);
+      if (i < n) xs[i] = tw_val(v[k]);
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -199,22 +327,24 @@ __device__ inline void stage_coh(const float* x, int n, float* xs) {
   }
 }
 
-// xs[i] = x[i] * rsqrt(mean(x^2) + eps) * (g ? g[i] : 1)
-__device__ inline void rmsnorm_stage(const float* x, const float* __restrict__ g, int n, float eps,
-                                     float* xs, float* red) {
+// xs[i] = x[i] * rsqrt(mean(x^2) + eps) * (g ? g[i] : 1), x tagged words
+template <int kB = 8>
+__device__ inline void rmsnorm_stage(const DevParams& p, const uint64_t* x, const float* __restrict__ g,
+                                     int n, const Sync& sy, float* xs, float* red) {
   __syncthreads();  // xs may still be read by a previous phase
-  stage_coh(x, n, xs);
-  __syncthreads();  // elements are staged in pairs by other threads
+  tw_stage<kB>(p, x, n, sy.tin, sy.poll, xs);
+  __syncthreads();
   float ss = 0.f;
   for (int i = threadIdx.x; i < n; i += kWG) ss = fmaf(xs[i], xs[i], ss);
-  const float r = rsqrtf(block_sum(ss, red) / static_cast<float>(n) + eps);
+  const float r = rsqrtf(block_sum(ss, red) / static_cast<float>(n) + p.eps);
   for (int i = threadIdx.x; i < n; i += kWG) xs[i] = xs[i] * r * (g ? g[i] : 1.f);
   __syncthreads();
 }
 
-__device__ inline void copy_stage(const float* x, int n, float* xs) {
+template <int kB = 8>
+__device__ inline void copy_stage(const DevParams& p, const uint64_t* x, int n, const Sync& sy, float* xs) {
   __syncthreads();
-  stage_coh(x, n, xs);
+  tw_stage<kB>(p, x, n, sy.tin, sy.poll, xs);
   __syncthreads();
 }
 
@@ -366,9 +496,12 @@ __device__ inline int64_t kv_offset(const DevParams& p, int l, int pos, int kvh)
 
 // Store the two outputs of row pair (r0, r0+1) of the repacked wqkv matrix:
 // q/k pairs are RoPE halves (i, i + D/2), rotated at position pos; v rows are
-// consecutive elements.
+// consecutive elements. q goes to its tagged vector; k and v go to the cache
+// and, when kvnew is set, also (storage-rounded) to the tagged copy of this
+// step's row that the attention phase reads.
 template <typename WT>
-__device__ inline void store_qkv_pair(const DevParams& p, int l, int pos, int r0, float x1, float x2) {
+__device__ inline void store_qkv_pair(const DevParams& p, int l, int pos, int r0, float x1, float x2,
+                                      uint32_t tag, bool kvnew) {
   const int AD = p.A * p.D, KD = p.K * p.D;
   if (r0 < AD + KD) {
     const int head = r0 / p.D;
@@ -379,21 +512,35 @@ __device__ inline void store_qkv_pair(const DevParams& p, int l, int pos, int r0
     const float y1 = x1 * c - x2 * s;
     const float y2 = x2 * c + x1 * s;
     if (r0 < AD) {
-      st_coh2(p.q + r0, y1, y2);
+      tw_store(p.q + r0, y1, tag);
+      tw_store(p.q + r0 + 1, y2, tag);
     } else {
       WT* kp = static_cast<WT*>(p.kpool) + kv_offset(p, l, pos, head - p.A) + rl;
       Elem<WT>::store_pair(kp, y1, y2);
+      if (kvnew) {
+        tw_store(p.kvnew + (r0 - AD), Elem<WT>::round(y1), tag);
+        tw_store(p.kvnew + (r0 - AD) + 1, Elem<WT>::round(y2), tag);
+      }
     }
   } else {
     const int j = r0 - AD - KD;
     const int kvh = j / p.D, d = j - kvh * p.D;
     WT* vp = static_cast<WT*>(p.vpool) + kv_offset(p, l, pos, kvh) + d;
     Elem<WT>::store_pair(vp, x1, x2);
+    if (kvnew) {
+      tw_store(p.kvnew + KD + j, Elem<WT>::round(x1), tag);
+      tw_store(p.kvnew + KD + j + 1, Elem<WT>::round(x2), tag);
+    }
   }
 }
 
-__device__ inline int step_token(const DevParams& p, int step) {
-  int tok = p.force_tok ? p.force_tok[step] : ld_coh(&p.ctl->next_token);
+// The input token of a step: forced, or emitted by the previous step (its
+// tagged record inside a persistent launch, the control record otherwise).
+__device__ inline int step_token(const DevParams& p, int step, const Sync& sy) {
+  int tok;
+  if (p.force_tok) tok = p.force_tok[step];
+  else if (sy.poll && step > 0) tok = __float_as_int(tw_val(tw_wait(p, p.dec + 1, sy.tres, true)));
+  else tok = ld_coh(&p.ctl->next_token);
   if (tok < 0 || tok >= p.V) {
     if (threadIdx.x == 0) atomicMax(&p.ctl->error, kErrToken);
     tok = 0;
@@ -421,12 +568,14 @@ struct QkvTask {
 
 template <typename WT, int CPL>
 __device__ void phase_qkv(const DevParams& p, int l, int pos, int step, int wg, int nwg, float* xs,
-                          float* red, QkvTask<WT, CPL>& t) {
+                          float* red, QkvTask<WT, CPL>& t, const Sync& sy) {
   const int pairs = p.qkv_rows >> 1;
   if (wg * kWaves >= pairs) return;
   const LayerW lw = p.layers[l];
   if (l == 0) {
-    const int tok = step_token(p, step);
+    // layer 0 starts from the token's embedding row; workgroup 0 also
+    // publishes it as the residual stream h
+    const int tok = step_token(p, step, sy);
     const WT* e = static_cast<const WT*>(p.embed) + static_cast<int64_t>(tok) * p.H;
     __syncthreads();
     float ss = 0.f;
@@ -434,14 +583,14 @@ __device__ void phase_qkv(const DevParams& p, int l, int pos, int step, int wg, 
       const float v = Elem<WT>::load(e + i);
       xs[i] = v;
       ss = fmaf(v, v, ss);
-      if (wg == 0) st_coh(p.h + i, v);
+      if (wg == 0) tw_store(p.h + i, v, sy.tout);
     }
     const float r = rsqrtf(block_sum(ss, red) / static_cast<float>(p.H) + p.eps);
     for (int i = threadIdx.x; i < p.H; i += kWG) xs[i] = xs[i] * r * lw.g_attn[i];
     __syncthreads();
-    if (wg == 0 && threadIdx.x == 0) st_coh(&p.ctl->exited, 0);
+    if (!sy.poll && wg == 0 && threadIdx.x == 0) st_coh(&p.ctl->exited, 0);
   } else {
-    rmsnorm_stage(p.h, lw.g_attn, p.H, p.eps, xs, red);
+    rmsnorm_stage(p, p.h, lw.g_attn, p.H, sy, xs, red);
   }
   const int nch = p.H / Elem<WT>::N;
   const int tw = nwg * kWaves;
@@ -451,7 +600,7 @@ __device__ void phase_qkv(const DevParams& p, int l, int pos, int step, int wg, 
     float acc[2];
     t.blk.dot(xs, 2, 0, nch, acc);
     wave_sum_n<2>(acc);
-    if ((threadIdx.x & 63) == 0) store_qkv_pair<WT>(p, l, pos, 2 * pair, acc[0], acc[1]);
+    if ((threadIdx.x & 63) == 0) store_qkv_pair<WT>(p, l, pos, 2 * pair, acc[0], acc[1], sy.tout, true);
   }
 }
 
@@ -589,15 +738,18 @@ struct AttnTask {
   }
   // After the barrier: the row of position pos (first item only).
   template <int LPP>
-  __device__ __forceinline__ void load_new(const DevParams& p, float* lds) {
+  // (from the tagged copy the projection phase wrote along with the cache)
+  __device__ __forceinline__ void load_new(const DevParams& p, int kvh, const Sync& sy) {
     if (!has_new) return;
     constexpr int PPW = 64 / LPP;
     const int lane = threadIdx.x & 63;
     const int sub = lane / LPP, dl = lane - sub * LPP;
     if (sub == nold % PPW) {
-      const int64_t o = offw(p, lds)[nold] + dl * N;
-      knew = *reinterpret_cast<const uint4*>(static_cast<const WT*>(p.kpool) + o);
-      vnew = *reinterpret_cast<const uint4*>(static_cast<const WT*>(p.vpool) + o);
+      const uint64_t* kw = p.kvnew + kvh * p.D + dl * N;
+      float kf[N], vf[N];
+      tw_read2<N>(p, kw, kw + p.K * p.D, sy.tin, sy.poll, kf, vf);
+      knew = Elem<WT>::pack(kf);
+      vnew = Elem<WT>::pack(vf);
     }
   }
   // the packed chunk of row slot k of this lane (the new row replaces the
@@ -616,7 +768,7 @@ struct AttnTask {
 
 template <typename WT, int LPP>
 __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, float* lds,
-                                          AttnTask<WT>& t) {
+                                          AttnTask<WT>& t, const Sync& sy) {
   constexpr int N = Elem<WT>::N;
   constexpr int PPW = 64 / LPP, RPL = kPosPerWave / PPW;
   const int T = pos + 1;
@@ -634,8 +786,8 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
   const int ws0 = sp * kAttnSplit + wave * kPosPerWave;
   const int wn = max(0, min(kPosPerWave, T - ws0));  // positions of this wave
   __syncthreads();
-  stage_coh(p.q + kvh * G * D, G * D, qs);
-  t.template load_new<LPP>(p, lds);
+  tw_stage<kMaxGroup * kMaxHeadDim / 2 / kWG>(p, p.q + kvh * G * D, G * D, sy.tin, sy.poll, qs);
+  t.template load_new<LPP>(p, kvh, sy);
   __syncthreads();
 
   if (wn > 0) {
@@ -750,7 +902,7 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
       num = fmaf(f, aw[w], num);
     }
     if (nsplit == 1) {
-      st_coh(p.o + kvh * G * D + idx, num / den);
+      tw_store(p.o + kvh * G * D + idx, num / den, sy.tout);
     } else {
       st_coh(pacc + (kvrec + sp) * G * D + idx, num);
       if (idx - g * D == 0) st_coh2(pml + ((kvrec + sp) * G + g) * 2, M, den);
@@ -763,7 +915,7 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
   if (threadIdx.x == 0) {
     const uint32_t old = __hip_atomic_fetch_add(&p.counters->attn[kvh][0], 1u, __ATOMIC_RELAXED,
                                                 __HIP_MEMORY_SCOPE_AGENT);
-    last_flag = (old == static_cast<uint32_t>(nsplit - 1));
+    last_flag = (old == sy.cbase + static_cast<uint32_t>(nsplit - 1));
   }
   __syncthreads();
   if (!last_flag) return;
@@ -822,9 +974,9 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
 #pragma unroll
   for (int k = 0; k < kIdx; ++k) {
     const int idx = static_cast<int>(threadIdx.x) + k * kWG;
-    if (idx < G * D) st_coh(p.o + kvh * G * D + idx, num[k] * fl[nsplit * G + idx / D]);
+    if (idx < G * D) tw_store(p.o + kvh * G * D + idx, num[k] * fl[nsplit * G + idx / D], sy.tout);
   }
-  if (threadIdx.x == 0)
+  if (!sy.poll && threadIdx.x == 0)
     __hip_atomic_store(&p.counters->attn[kvh][0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -833,7 +985,7 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
 // all of theirs after the barrier.
 template <typename WT, int LPP>
 __device__ __forceinline__ void phase_attn(const DevParams& p, int l, int pos, int wg, int nwg,
-                                           float* lds, AttnTask<WT>& t) {
+                                           float* lds, AttnTask<WT>& t, const Sync& sy) {
   const int nsplit = (pos + kAttnSplit) / kAttnSplit;
   const int items = p.K * nsplit;
   for (int it = wg; it < items; it += nwg) {
@@ -841,11 +993,11 @@ __device__ __forceinline__ void phase_attn(const DevParams& p, int l, int pos, i
       __syncthreads();  // offsets of the previous item may still be read
       t.offsets(p, l, pos, it, nsplit, lds);
       const int ws0 = (it % nsplit) * kAttnSplit + wave_id() * kPosPerWave;
-      t.nold = max(0, min(kPosPerWave, pos + 1 - ws0));
-      t.has_new = false;
+      t.nold = max(0, min(kPosPerWave, pos - ws0));
+      t.has_new = pos >= ws0 && pos < ws0 + kPosPerWave;  // read from its tagged copy
       t.template load_old<LPP>(p, AttnTask<WT>::offw(p, lds), t.nold);
     }
-    attn_item<WT, LPP>(p, pos, it, lds, t);
+    attn_item<WT, LPP>(p, pos, it, lds, t, sy);
   }
 }
 
@@ -863,21 +1015,26 @@ struct RowTask {
 };
 
 template <typename WT, int CPL>
-__device__ void phase_rows(const WT* W, int rows, int cols, const float* x, float* out,
-                           const float* bias, int residual, int wg, int nwg, float* xs,
-                           RowTask<WT, CPL>& t) {
+__device__ void phase_rows(const DevParams& p, const WT* W, int rows, int cols, const uint64_t* x,
+                           uint64_t* out, const float* bias, int residual, int wg, int nwg, float* xs,
+                           RowTask<WT, CPL>& t, const Sync& sy) {
   if (wg * kWaves >= rows) return;
-  copy_stage(x, cols, xs);
+  const int r0 = wg * kWaves + wave_id();
+  // the residual of the wave's first row is read before the input is staged
+  float prev0 = 0.f;
+  if (residual && (threadIdx.x & 63) == 0 && r0 < rows) prev0 = tw_val(tw_wait(p, out + r0, sy.tres, sy.poll));
+  copy_stage(p, x, cols, sy, xs);
   const int nch = cols / Elem<WT>::N;
   const int tw = nwg * kWaves;
-  for (int r = wg * kWaves + wave_id(); r < rows; r += tw) {
-    if (r != wg * kWaves + wave_id()) t.blk.load(W, cols, r, 1, 0, nch);
+  for (int r = r0; r < rows; r += tw) {
+    if (r != r0) t.blk.load(W, cols, r, 1, 0, nch);
     float acc[1];
     t.blk.dot(xs, 1, 0, nch, acc);
     acc[0] = wave_sum(acc[0]);
     if ((threadIdx.x & 63) == 0) {
-      const float prev = residual ? ld_coh(out + r) : (bias ? bias[r] : 0.f);
-      st_coh(out + r, prev + acc[0]);
+      float prev = bias ? bias[r] : 0.f;
+      if (residual) prev = r == r0 ? prev0 : tw_val(tw_wait(p, out + r, sy.tres, sy.poll));
+      tw_store(out + r, prev + acc[0], sy.tout);
     }
   }
 }
@@ -913,19 +1070,19 @@ __device__ inline float silu(float x) { return x / (1.f + expf(-x)); }
 
 template <typename WT, int CPL>
 __device__ void phase_gateup(const DevParams& p, int l, int wg, int nwg, float* xs, float* red,
-                             GateUpTask<WT, CPL>& t) {
+                             GateUpTask<WT, CPL>& t, const Sync& sy) {
   const int tw = nwg * kWaves;
   const int gw0 = wg * kWaves;
   if (gu_begin(p, gw0 + kWaves, tw) == gu_begin(p, gw0, tw)) return;
   const LayerW lw = p.layers[l];
-  rmsnorm_stage(p.h, lw.g_mlp, p.H, p.eps, xs, red);
-  float* a_out = p.a;
+  rmsnorm_stage(p, p.h, lw.g_mlp, p.H, sy, xs, red);
+  uint64_t* a_out = p.a;
   stream_tiles<WT, kRS, CPL>(static_cast<const WT*>(lw.wgu), p.H, GateUpTask<WT, CPL>::tiling(p, wg, nwg),
                              xs, t.a, t.b, [&](int r0, int nr, const float(&acc)[kRS]) {
                               if ((threadIdx.x & 63) == 0) {
 #pragma unroll
                                 for (int i = 0; i < kRS / 2; ++i)
-                                  if (2 * i < nr) st_coh(a_out + r0 / 2 + i, silu(acc[2 * i]) * acc[2 * i + 1]);
+                                  if (2 * i < nr) tw_store(a_out + r0 / 2 + i, silu(acc[2 * i]) * acc[2 * i + 1], sy.tout);
                               }
                             }, 2);
 }
@@ -948,27 +1105,27 @@ struct DownTask {
                                 nch * wave_id() / kWaves, nch * (wave_id() + 1) / kWaves,
                                 max(1, (longest + 64 * CPL - 1) / (64 * CPL))};
   }
-  // Before the barrier: the first two tiles, and the residual rows (h is
-  // last written by the output projection, two barriers earlier).
-  __device__ __forceinline__ void prefetch(const DevParams& p, int l, int wg, int nwg) {
+  // Before the input is ready: the first two tiles, and the residual rows (h
+  // is last written by the output projection, before the gate/up phase).
+  __device__ __forceinline__ void prefetch(const DevParams& p, int l, int wg, int nwg, const Sync& sy) {
     const auto tl = tiling(p, wg, nwg);
     const WT* W = static_cast<const WT*>(p.layers[l].wd);
     if (tl.count() > 0) tl.load(a, W, p.F, 0);
     if (tl.count() > 1) tl.load(b, W, p.F, 1);
     const int r = tl.rb + static_cast<int>(threadIdx.x);
-    hres = r < tl.re ? ld_coh(p.h + r) : 0.f;
+    hres = r < tl.re ? tw_val(tw_wait(p, p.h + r, sy.tres, sy.poll)) : 0.f;
   }
 };
 
 template <typename WT, int CPL>
 __device__ void phase_down(const DevParams& p, int l, int wg, int nwg, float* xs, float* red,
-                           DownTask<WT, CPL>& t) {
+                           DownTask<WT, CPL>& t, const Sync& sy) {
   const auto tl = DownTask<WT, CPL>::tiling(p, wg, nwg);
   if (tl.rb >= tl.re) return;
-  copy_stage(p.a, p.F, xs);
+  copy_stage<18>(p, p.a, p.F, sy, xs);
   const int wave = wave_id();
   const int tid = threadIdx.x;
-  float* h = p.h;
+  uint64_t* h = p.h;
   stream_tiles<WT, kRS, CPL>(static_cast<const WT*>(p.layers[l].wd), p.F, tl, xs, t.a, t.b,
                              [&](int r0, int nr, const float(&acc)[kRS]) {
                                if ((tid & 63) == 0) {
@@ -981,11 +1138,12 @@ __device__ void phase_down(const DevParams& p, int l, int wg, int nwg, float* xs
                                if (i >= 0 && i < nr) {
                                  float sum = 0.f;
                                  for (int w = 0; w < kWaves; ++w) sum += red[w * kRS + i];
-                                 st_coh(h + r0 + i, t.hres + sum);
+                                 tw_store(h + r0 + i, t.hres + sum, sy.tout);
                                } else if (r0 - tl.rb + nr > kWG && tid < nr && r0 - tl.rb + tid >= kWG) {
                                  float sum = 0.f;
                                  for (int w = 0; w < kWaves; ++w) sum += red[w * kRS + tid];
-                                 st_coh(h + r0 + tid, ld_coh(h + r0 + tid) + sum);
+                                 const float prev = tw_val(tw_wait(p, h + r0 + tid, sy.tres, sy.poll));
+                                 tw_store(h + r0 + tid, prev + sum, sy.tout);
                                }
                                __syncthreads();
                              }, 2);
@@ -1056,8 +1214,8 @@ struct HeadTask {
 
 template <typename WT, int CPL, int R = kRS>
 __device__ void phase_head(const DevParams& p, int readout, int step, int wg, int nwg, float* xs,
-                           float* red, HeadTask<WT, CPL, R>& t) {
-  rmsnorm_stage(readout ? p.z : p.h, p.g_final, p.H, p.eps, xs, red);
+                           float* red, HeadTask<WT, CPL, R>& t, const Sync& sy) {
+  rmsnorm_stage(p, readout ? p.z : p.h, p.g_final, p.H, sy, xs, red);
   float* dbg = readout ? p.dbg_logits_r : p.dbg_logits_f;
   const int wave = wave_id(), lane = threadIdx.x & 63;
   Stat st = stat_empty();
@@ -1089,18 +1247,29 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
     wait_stores();
     const uint32_t old = __hip_atomic_fetch_add(&p.counters->head[0], 1u, __ATOMIC_RELAXED,
                                                 __HIP_MEMORY_SCOPE_AGENT);
-    last_flag = (old == static_cast<uint32_t>(nwg - 1));
+    last_flag = (old == sy.cbase + static_cast<uint32_t>(nwg - 1));
   }
   __syncthreads();
   if (!last_flag) return;
+  // the partials of up to 4 * kWG workgroups are loaded before any is merged
   Stat tt = stat_empty();
-  for (int i = threadIdx.x; i < nwg; i += kWG) {
-    const float* part = p.head_part + static_cast<int64_t>(i) * 4;
-    const uint64_t a = ld_coh_u64(part), b = ld_coh_u64(part + 2);
-    tt = stat_merge(tt, Stat{__uint_as_float(static_cast<uint32_t>(a)),
-                             __uint_as_float(static_cast<uint32_t>(a >> 32)),
-                             __uint_as_float(static_cast<uint32_t>(b)),
-                             static_cast<int>(static_cast<uint32_t>(b >> 32))});
+  for (int i0 = 0; i0 < nwg; i0 += 4 * kWG) {
+    uint64_t a[4], b[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int i = i0 + k * kWG + static_cast<int>(threadIdx.x);
+      const float* part = p.head_part + static_cast<int64_t>(min(i, nwg - 1)) * 4;
+      a[k] = ld_coh_u64(part);
+      b[k] = ld_coh_u64(part + 2);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (i0 + k * kWG + static_cast<int>(threadIdx.x) < nwg)
+        tt = stat_merge(tt, Stat{__uint_as_float(static_cast<uint32_t>(a[k])),
+                                 __uint_as_float(static_cast<uint32_t>(a[k] >> 32)),
+                                 __uint_as_float(static_cast<uint32_t>(b[k])),
+                                 static_cast<int>(static_cast<uint32_t>(b[k] >> 32))});
+    }
   }
   stl[threadIdx.x * 4 + 0] = tt.m;
   stl[threadIdx.x * 4 + 1] = tt.s;
@@ -1125,11 +1294,17 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
     const int idx = __float_as_int(stl[3]);
     const float conf = 1.f / stl[1];
     StepCtl* c = p.ctl;
-    __hip_atomic_store(&p.counters->head[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (!sy.poll)
+      __hip_atomic_store(&p.counters->head[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (readout) {
       const int would = conf > p.tau;
       const int fe = p.force_exit ? p.force_exit[step] : -1;
       const int ex = fe < 0 ? would : fe;
+      // the gate record every workgroup reads: exited, token, confidence, decision
+      tw_store(p.dec + 2, conf, sy.tout);
+      tw_store(p.dec + 3, __int_as_float(would), sy.tout);
+      if (ex) tw_store(p.dec + 1, __int_as_float(idx), sy.tout);
+      tw_store(p.dec + 0, __int_as_float(ex), sy.tout);
       st_coh(&c->readout_token, idx);
       st_coh(&c->conf, conf);
       st_coh(&c->would_exit, would);
@@ -1145,14 +1320,24 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
       }
     } else {
       const int gated = p.exit_layer > 0;
+      tw_store(p.dec + 1, __int_as_float(idx), sy.tout);
       st_coh(&c->full_token, idx);
       st_coh(&c->conf_full, conf);
       st_coh(&c->next_token, idx);
       if (p.ring_tok) {
+        float rconf = conf;
+        int rwould = 0;
+        if (gated && sy.poll) {  // this step's gate record (tag sy.tres)
+          rconf = tw_val(tw_wait(p, p.dec + 2, sy.tres, true));
+          rwould = __float_as_int(tw_val(tw_wait(p, p.dec + 3, sy.tres, true)));
+        } else if (gated) {
+          rconf = ld_coh(&c->conf);
+          rwould = ld_coh(&c->would_exit);
+        }
         p.ring_tok[step] = idx;
         p.ring_exit[step] = 0;
-        p.ring_conf[step] = gated ? ld_coh(&c->conf) : conf;
-        p.ring_would[step] = gated ? ld_coh(&c->would_exit) : 0;
+        p.ring_conf[step] = rconf;
+        p.ring_would[step] = rwould;
       }
     }
   }
@@ -1166,11 +1351,12 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
 // each layer's gain is applied chunk by chunk.
 // ---------------------------------------------------------------------------
 template <typename WT, int CPL>
-__device__ void phase_fill(const DevParams& p, int pos, int wg, int nwg, float* xs, float* red) {
+__device__ void phase_fill(const DevParams& p, int pos, int wg, int nwg, float* xs, float* red,
+                           const Sync& sy) {
   const int KD = p.K * p.D;  // row pairs per layer (k and v rows: 2*KD)
   const int total = (p.L - p.exit_layer) * KD;
   if (wg * kWaves >= total) return;
-  rmsnorm_stage(p.h_exit, nullptr, p.H, p.eps, xs, red);
+  rmsnorm_stage(p, p.h_exit, nullptr, p.H, sy, xs, red);
   const int nch = p.H / Elem<WT>::N;
   const int tw = nwg * kWaves;
   RowBlock<WT, 2, CPL> blk;
@@ -1182,20 +1368,19 @@ __device__ void phase_fill(const DevParams& p, int pos, int wg, int nwg, float* 
     float acc[2];
     blk.dot_gain(xs, lw.g_attn, 2, 0, nch, acc);
     wave_sum_n<2>(acc);
-    if ((threadIdx.x & 63) == 0) store_qkv_pair<WT>(p, l, pos, r0, acc[0], acc[1]);
+    if ((threadIdx.x & 63) == 0) store_qkv_pair<WT>(p, l, pos, r0, acc[0], acc[1], sy.tout, false);
   }
 }
 
 // readout: z = W_r h + b_r; workgroup 0 also keeps h as h_exit.
 template <typename WT, int CPL>
-__device__ void phase_readout(const DevParams& p, int wg, int nwg, float* xs, RowTask<WT, CPL>& t) {
+__device__ void phase_readout(const DevParams& p, int wg, int nwg, float* xs, RowTask<WT, CPL>& t,
+                              const Sync& sy) {
   if (wg == 0) {
-    for (int i = threadIdx.x * 2; i < p.H; i += kWG * 2) {
-      const uint64_t v = ld_coh_u64(p.h + i);
-      st_coh_u64(p.h_exit + i, v);
-    }
+    for (int i = threadIdx.x; i < p.H; i += kWG)
+      tw_store(p.h_exit + i, tw_val(tw_wait(p, p.h + i, sy.tin, sy.poll)), sy.tout);
   }
-  phase_rows<WT, CPL>(static_cast<const WT*>(p.ro_w), p.H, p.H, p.h, p.z, p.ro_b, 0, wg, nwg, xs, t);
+  phase_rows<WT, CPL>(p, static_cast<const WT*>(p.ro_w), p.H, p.H, p.h, p.z, p.ro_b, 0, wg, nwg, xs, t, sy);
 }
 
 size_t lds_bytes(const DevParams& p) {
@@ -1224,49 +1409,50 @@ __global__ __launch_bounds__(kWG) void k_op(DevParams p, int l, int pos, int ste
   if (skip_if_exited && ld_coh(&p.ctl->exited)) return;
   const Lds s = lds_carve(p, smem);
   const int wg = blockIdx.x, nwg = gridDim.x;
+  const Sync sy{false, 0u, 0u, 0u, 0u};  // kernel boundaries order the operations
   if constexpr (OP == kOpQkv) {
     QkvTask<WT, CPL> t;
     t.prefetch(p, l, wg);
-    phase_qkv<WT, CPL>(p, l, pos, step, wg, nwg, s.xs, s.red, t);
+    phase_qkv<WT, CPL>(p, l, pos, step, wg, nwg, s.xs, s.red, t, sy);
   }
   if constexpr (OP == kOpAttn) {
     AttnTask<WT> t;
     if (attn_row_chunks<WT>(p) == 16) {
       t.template prefetch<16>(p, l, pos, wg, s.xs);
-      phase_attn<WT, 16>(p, l, pos, wg, nwg, s.xs, t);
+      phase_attn<WT, 16>(p, l, pos, wg, nwg, s.xs, t, sy);
     } else {
       t.template prefetch<8>(p, l, pos, wg, s.xs);
-      phase_attn<WT, 8>(p, l, pos, wg, nwg, s.xs, t);
+      phase_attn<WT, 8>(p, l, pos, wg, nwg, s.xs, t, sy);
     }
   }
   if constexpr (OP == kOpWo) {
     const WT* W = static_cast<const WT*>(p.layers[l].wo);
     RowTask<WT, CPL> t;
     t.prefetch(W, p.H, p.A * p.D, wg);
-    phase_rows<WT, CPL>(W, p.H, p.A * p.D, p.o, p.h, nullptr, 1, wg, nwg, s.xs, t);
+    phase_rows<WT, CPL>(p, W, p.H, p.A * p.D, p.o, p.h, nullptr, 1, wg, nwg, s.xs, t, sy);
   }
   if constexpr (OP == kOpGateUp) {
     GateUpTask<WT, CPL> t;
     t.prefetch(p, l, wg, nwg);
-    phase_gateup<WT, CPL>(p, l, wg, nwg, s.xs, s.red, t);
+    phase_gateup<WT, CPL>(p, l, wg, nwg, s.xs, s.red, t, sy);
   }
   if constexpr (OP == kOpDown) {
     DownTask<WT, CPL> t;
-    t.prefetch(p, l, wg, nwg);
-    phase_down<WT, CPL>(p, l, wg, nwg, s.xs, s.red, t);
+    t.prefetch(p, l, wg, nwg, sy);
+    phase_down<WT, CPL>(p, l, wg, nwg, s.xs, s.red, t, sy);
   }
   if constexpr (OP == kOpReadout) {
     RowTask<WT, CPL> t;
     t.prefetch(static_cast<const WT*>(p.ro_w), p.H, p.H, wg);
-    phase_readout<WT, CPL>(p, wg, nwg, s.xs, t);
+    phase_readout<WT, CPL>(p, wg, nwg, s.xs, t, sy);
   }
   if constexpr (OP == kOpHeadR || OP == kOpHeadF) {
     HeadTask<WT, CPL> t;
     t.prefetch(p, wg, nwg);
-    phase_head<WT, CPL>(p, OP == kOpHeadR, step, wg, nwg, s.xs, s.red, t);
+    phase_head<WT, CPL>(p, OP == kOpHeadR, step, wg, nwg, s.xs, s.red, t, sy);
   }
   if constexpr (OP == kOpFill)
-    if (ld_coh(&p.ctl->exited)) phase_fill<WT, CPL>(p, pos, wg, nwg, s.xs, s.red);
+    if (ld_coh(&p.ctl->exited)) phase_fill<WT, CPL>(p, pos, wg, nwg, s.xs, s.red, sy);
 }
 
 static int op_grid(const DevParams& p, int op, int pos, int head_wgs) {
@@ -1344,8 +1530,6 @@ static hipError_t step_per_op(const DevParams& p, int pos, int step, int emit_he
 // ---------------------------------------------------------------------------
 // persistent cooperative kernel: n whole decode steps in one launch
 // ---------------------------------------------------------------------------
-constexpr uint64_t kWaitTicks = 400000000ull;  // ~4 s of the 100 MHz wall clock
-
 // Two-level grid barrier, split in arrive and wait so that a workgroup can
 // issue the next phase's weight loads in between. Epochs count barriers of
 // the launch; wait() for an epoch already reached returns at once. The wait
@@ -1393,119 +1577,156 @@ __device__ inline void bar_wait(const DevParams& p, uint32_t epoch) {
   __syncthreads();
 }
 
-// The steps of the persistent program; each returns the updated barrier epoch.
-// Each reads the workgroup index through an opaque scalar move: values derived
-// from it (row ranges, weight pointers) are then computed inside the step
-// rather than hoisted out of the step and layer loops, where the invariants of
-// every phase would otherwise stay live together and exhaust the registers.
+// The steps of the persistent program. Tags holds, identically in every
+// workgroup (the control flow is uniform), the tag of the latest version of
+// each vector and the arrivals counted so far on the last-arriver counters.
+struct Tags {
+  uint32_t ep;                 // phases run in this launch; phase e writes tag e
+  uint32_t h, q, o, a, z, hx;  // latest version of each vector
+  uint32_t gate;               // latest gate record (readout head)
+  uint32_t tok;                // record holding the next input token
+  uint32_t attn;               // arrivals per KV head on the attention counter
+  uint32_t heads;              // head phases run
+};
+
+__device__ __forceinline__ void tl_mark(const DevParams& p, uint32_t idx) {
+  if (p.timeline && blockIdx.x == 0 && threadIdx.x == 0 && static_cast<int>(idx) < p.timeline_cap)
+    p.timeline[idx] = wall_clock64();
+}
+
+// Each step reads the workgroup index through an opaque scalar move: values
+// derived from it (row ranges, weight pointers) are then computed inside the
+// step rather than hoisted out of the step and layer loops, where the
+// invariants of every phase would otherwise stay live together and exhaust
+// the registers.
 __device__ __forceinline__ int opaque_wg() {
   int v;
   asm volatile("s_mov_b32 %0, %1" : "=s"(v) : "s"(static_cast<int>(blockIdx.x)));
   return v;
 }
-#define EE_PHASE_FN template <typename WT, int CPL> __device__ __forceinline__ uint32_t
+#define EE_PHASE_FN template <typename WT, int CPL> __device__ __forceinline__ void
 
-EE_PHASE_FN run_qkv(const DevParams& p, int l, int pos, int step, float* smem, uint32_t ep) {
+EE_PHASE_FN run_qkv(const DevParams& p, int l, int pos, int step, float* smem, Tags& tg) {
   const int wg = opaque_wg();
   const Lds s = lds_carve(p, smem);
   QkvTask<WT, CPL> t;
   t.prefetch(p, l, wg);
-  bar_wait(p, ep);
-  phase_qkv<WT, CPL>(p, l, pos, step, wg, gridDim.x, s.xs, s.red, t);
-  bar_arrive(p, ep, wg, gridDim.x);
-  return ep;
+  const uint32_t E = ++tg.ep;
+  tl_mark(p, 2 * E);
+  phase_qkv<WT, CPL>(p, l, pos, step, wg, gridDim.x, s.xs, s.red, t, Sync{true, tg.h, tg.tok, E, 0u});
+  tl_mark(p, 2 * E + 1);
+  tg.q = E;
+  if (l == 0) tg.h = E;
 }
 
-EE_PHASE_FN run_attn(const DevParams& p, int l, int pos, float* smem, uint32_t ep) {
+EE_PHASE_FN run_attn(const DevParams& p, int l, int pos, float* smem, Tags& tg) {
   const int wg = opaque_wg();
   AttnTask<WT> t;
+  // the prefetch writes row offsets into LDS, which waves of this workgroup
+  // may still be reading as the projection phase's input
+  __syncthreads();
+  const uint32_t E = ++tg.ep;
+  const Sync sy{true, tg.q, 0u, E, tg.attn};
   if (attn_row_chunks<WT>(p) == 16) {
     t.template prefetch<16>(p, l, pos, wg, smem);
-    bar_wait(p, ep);
-    phase_attn<WT, 16>(p, l, pos, wg, gridDim.x, smem, t);
+    tl_mark(p, 2 * E);
+    phase_attn<WT, 16>(p, l, pos, wg, gridDim.x, smem, t, sy);
   } else {
     t.template prefetch<8>(p, l, pos, wg, smem);
-    bar_wait(p, ep);
-    phase_attn<WT, 8>(p, l, pos, wg, gridDim.x, smem, t);
+    tl_mark(p, 2 * E);
+    phase_attn<WT, 8>(p, l, pos, wg, gridDim.x, smem, t, sy);
   }
-  bar_arrive(p, ep, wg, gridDim.x);
-  return ep;
+  tl_mark(p, 2 * E + 1);
+  tg.o = E;
+  // a single split writes o itself and never arrives on the counter
+  const int nsplit = (pos + kAttnSplit) / kAttnSplit;
+  if (nsplit > 1) tg.attn += static_cast<uint32_t>(nsplit);
 }
 
-EE_PHASE_FN run_wo(const DevParams& p, int l, float* smem, uint32_t ep) {
+EE_PHASE_FN run_wo(const DevParams& p, int l, float* smem, Tags& tg) {
   const int wg = opaque_wg();
   const Lds s = lds_carve(p, smem);
   const WT* W = static_cast<const WT*>(p.layers[l].wo);
   RowTask<WT, CPL> t;
   t.prefetch(W, p.H, p.A * p.D, wg);
-  bar_wait(p, ep);
-  phase_rows<WT, CPL>(W, p.H, p.A * p.D, p.o, p.h, nullptr, 1, wg, gridDim.x, s.xs, t);
-  bar_arrive(p, ep, wg, gridDim.x);
-  return ep;
+  const uint32_t E = ++tg.ep;
+  tl_mark(p, 2 * E);
+  phase_rows<WT, CPL>(p, W, p.H, p.A * p.D, p.o, p.h, nullptr, 1, wg, gridDim.x, s.xs, t,
+                      Sync{true, tg.o, tg.h, E, 0u});
+  tl_mark(p, 2 * E + 1);
+  tg.h = E;
 }
 
-EE_PHASE_FN run_gateup(const DevParams& p, int l, float* smem, uint32_t ep) {
+EE_PHASE_FN run_gateup(const DevParams& p, int l, float* smem, Tags& tg) {
   const int wg = opaque_wg();
   const Lds s = lds_carve(p, smem);
   GateUpTask<WT, CPL> t;
   t.prefetch(p, l, wg, gridDim.x);
-  bar_wait(p, ep);
-  phase_gateup<WT, CPL>(p, l, wg, gridDim.x, s.xs, s.red, t);
-  bar_arrive(p, ep, wg, gridDim.x);
-  return ep;
+  const uint32_t E = ++tg.ep;
+  tl_mark(p, 2 * E);
+  phase_gateup<WT, CPL>(p, l, wg, gridDim.x, s.xs, s.red, t, Sync{true, tg.h, 0u, E, 0u});
+  tl_mark(p, 2 * E + 1);
+  tg.a = E;
 }
 
-EE_PHASE_FN run_down(const DevParams& p, int l, float* smem, uint32_t ep) {
+EE_PHASE_FN run_down(const DevParams& p, int l, float* smem, Tags& tg) {
   const int wg = opaque_wg();
   const Lds s = lds_carve(p, smem);
+  const uint32_t E = ++tg.ep;
+  const Sync sy{true, tg.a, tg.h, E, 0u};
   DownTask<WT, CPL> t;
-  t.prefetch(p, l, wg, gridDim.x);
-  bar_wait(p, ep);
-  phase_down<WT, CPL>(p, l, wg, gridDim.x, s.xs, s.red, t);
-  bar_arrive(p, ep, wg, gridDim.x);
-  return ep;
+  t.prefetch(p, l, wg, gridDim.x, sy);
+  tl_mark(p, 2 * E);
+  phase_down<WT, CPL>(p, l, wg, gridDim.x, s.xs, s.red, t, sy);
+  tl_mark(p, 2 * E + 1);
+  tg.h = E;
 }
 
-EE_PHASE_FN run_readout(const DevParams& p, float* smem, uint32_t ep) {
+EE_PHASE_FN run_readout(const DevParams& p, float* smem, Tags& tg) {
   const int wg = opaque_wg();
   const Lds s = lds_carve(p, smem);
   RowTask<WT, CPL> t;
   t.prefetch(static_cast<const WT*>(p.ro_w), p.H, p.H, wg);
-  bar_wait(p, ep);
-  phase_readout<WT, CPL>(p, wg, gridDim.x, s.xs, t);
-  bar_arrive(p, ep, wg, gridDim.x);
-  return ep;
+  const uint32_t E = ++tg.ep;
+  tl_mark(p, 2 * E);
+  phase_readout<WT, CPL>(p, wg, gridDim.x, s.xs, t, Sync{true, tg.h, 0u, E, 0u});
+  tl_mark(p, 2 * E + 1);
+  tg.z = E;
+  tg.hx = E;
 }
 
-EE_PHASE_FN run_head(const DevParams& p, int readout, int step, float* smem, uint32_t ep) {
+EE_PHASE_FN run_head(const DevParams& p, int readout, int step, float* smem, Tags& tg) {
   const int wg = opaque_wg();
   const Lds s = lds_carve(p, smem);
   HeadTask<WT, CPL> t;
   t.prefetch(p, wg, gridDim.x);
-  bar_wait(p, ep);
-  phase_head<WT, CPL>(p, readout, step, wg, gridDim.x, s.xs, s.red, t);
-  bar_arrive(p, ep, wg, gridDim.x);
-  return ep;
+  const uint32_t E = ++tg.ep;
+  tl_mark(p, 2 * E);
+  phase_head<WT, CPL>(p, readout, step, wg, gridDim.x, s.xs, s.red, t,
+                      Sync{true, readout ? tg.z : tg.h, tg.gate, E, tg.heads * gridDim.x});
+  tl_mark(p, 2 * E + 1);
+  ++tg.heads;
+  if (readout) tg.gate = E;
 }
 
-EE_PHASE_FN run_fill(const DevParams& p, int pos, float* smem, uint32_t ep) {
+EE_PHASE_FN run_fill(const DevParams& p, int pos, float* smem, Tags& tg) {
   const int wg = opaque_wg();
   const Lds s = lds_carve(p, smem);
-  bar_wait(p, ep);
-  phase_fill<WT, CPL>(p, pos, wg, gridDim.x, s.xs, s.red);
-  bar_arrive(p, ep, wg, gridDim.x);
-  return ep;
+  const uint32_t E = ++tg.ep;
+  tl_mark(p, 2 * E);
+  phase_fill<WT, CPL>(p, pos, wg, gridDim.x, s.xs, s.red, Sync{true, tg.hx, 0u, E, 0u});
+  tl_mark(p, 2 * E + 1);
 }
 #undef EE_PHASE_FN
 
 template <typename WT, int CPL>
-__device__ __forceinline__ uint32_t run_layer(const DevParams& p, int l, int pos, int step, float* smem,
-                                              uint32_t ep) {
-  ep = run_qkv<WT, CPL>(p, l, pos, step, smem, ep);
-  ep = run_attn<WT, CPL>(p, l, pos, smem, ep);
-  ep = run_wo<WT, CPL>(p, l, smem, ep);
-  ep = run_gateup<WT, CPL>(p, l, smem, ep);
-  return run_down<WT, CPL>(p, l, smem, ep);
+__device__ __forceinline__ void run_layer(const DevParams& p, int l, int pos, int step, float* smem,
+                                          Tags& tg) {
+  run_qkv<WT, CPL>(p, l, pos, step, smem, tg);
+  run_attn<WT, CPL>(p, l, pos, smem, tg);
+  run_wo<WT, CPL>(p, l, smem, tg);
+  run_gateup<WT, CPL>(p, l, smem, tg);
+  run_down<WT, CPL>(p, l, smem, tg);
 }
 
 // Parameters of the persistent kernel live in constant memory, one slot per
@@ -1517,48 +1738,78 @@ __constant__ DevParams c_params[kParamSlots];
 // prefill != 0: prompt positions, ungated, head only at the last position.
 // One loop over the layers (a single inlined copy of the layer code); the
 // readout and the gate run after layer exit_layer, and an exit leaves the
-// loop for the KV fill of the remaining layers.
+// loop for the KV fill of the remaining layers. Every step ends with a grid
+// barrier: the next step reads KV rows this step wrote (the fill's included),
+// and with forced tokens nothing else orders the two steps.
 template <typename WT, int CPL>
 __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_decode_persistent(
     int slot, int pos0, int n, int prefill) {
   extern __shared__ float smem[];
+  __shared__ int sh_exited;
   const DevParams& p = c_params[slot];
-  uint32_t ep = 0;
+  Tags tg{};
+  uint32_t bep = 0;
   const int Le = p.exit_layer;
   for (int i = 0; i < n; ++i) {
-    if (__hip_atomic_load(&p.ctl->abort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) break;
+    if (aborted(p)) break;
     const int pos = pos0 + i;
     int exited = 0;
     for (int l = 0; l < p.L; ++l) {
-      ep = run_layer<WT, CPL>(p, l, pos, i, smem, ep);
+      run_layer<WT, CPL>(p, l, pos, i, smem, tg);
       if (l + 1 == Le) {
-        ep = run_readout<WT, CPL>(p, smem, ep);
-        ep = run_head<WT, CPL>(p, 1, i, smem, ep);
-        bar_wait(p, ep);
-        exited = ld_coh(&p.ctl->exited);
-        if (exited) break;
+        run_readout<WT, CPL>(p, smem, tg);
+        run_head<WT, CPL>(p, 1, i, smem, tg);
+        __syncthreads();
+        if (threadIdx.x == 0) sh_exited = __float_as_int(tw_val(tw_wait(p, p.dec, tg.gate, true)));
+        __syncthreads();
+        exited = sh_exited;
+        if (exited) {
+          tg.tok = tg.gate;
+          break;
+        }
       }
     }
     if (exited) {
-      if (Le < p.L) ep = run_fill<WT, CPL>(p, pos, smem, ep);
+      if (Le < p.L) run_fill<WT, CPL>(p, pos, smem, tg);
     } else if (!prefill || i == n - 1) {
-      ep = run_head<WT, CPL>(p, 0, i, smem, ep);
+      run_head<WT, CPL>(p, 0, i, smem, tg);
+      tg.tok = tg.ep;
+    }
+    bar_arrive(p, bep, blockIdx.x, gridDim.x);
+    bar_wait(p, bep);
+  }
+}
+
+// Launch state of the persistent kernel: barrier and last-arriver counters,
+// and every tagged word (tag 0 is never written inside a launch).
+__global__ __launch_bounds__(kWG) void k_reset_state(Counters* c, uint64_t* tw, int64_t nw) {
+  const int t = threadIdx.x;
+  if (blockIdx.x == 0) {
+    if (t < kBarGroups) c->group[t][0] = 0u;
+    if (t < 16) c->attn[t][0] = 0u;
+    if (t == 0) {
+      c->top[0] = 0u;
+      c->gen[0] = 0u;
+      c->head[0] = 0u;
     }
   }
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kWG + t; i < nw; i += static_cast<int64_t>(gridDim.x) * kWG)
+    tw[i] = 0ull;
 }
 
-__global__ void k_reset_barrier(Counters* c) {
-  const int t = threadIdx.x;
-  if (t < kBarGroups) c->group[t][0] = 0u;
-  if (t == 0) {
-    c->top[0] = 0u;
-    c->gen[0] = 0u;
-  }
+__global__ __launch_bounds__(kWG) void k_tag_vec(uint64_t* dst, const float* src, int n) {
+  for (int i = blockIdx.x * kWG + threadIdx.x; i < n; i += gridDim.x * kWG) dst[i] = tw_pack(src[i], 0u);
 }
 
-__global__ __launch_bounds__(kWG) void k_copy_vec(float* dst, const float* src, int n) {
-  for (int i = blockIdx.x * kWG + threadIdx.x; i < n; i += gridDim.x * kWG) dst[i] = src[i];
+__global__ __launch_bounds__(kWG) void k_untag(float* dst, const uint64_t* src, int n) {
+  for (int i = blockIdx.x * kWG + threadIdx.x; i < n; i += gridDim.x * kWG) dst[i] = tw_val(src[i]);
 }
+
+hipError_t launch_untag(float* dst, const uint64_t* src, int n, hipStream_t s) {
+  hipLaunchKernelGGL(k_untag, dim3(8), dim3(kWG), 0, s, dst, src, n);
+  return hipGetLastError();
+}
+
 
 // ---------------------------------------------------------------------------
 // host dispatch over (storage type, chunks per lane)
@@ -1586,8 +1837,17 @@ static hipError_t dispatch(int wbf16, int cpl, F&& f) {
   return hipErrorInvalidValue;
 }
 
+// one kernel per operation relies on counters that start at zero (a
+// persistent launch leaves them counting)
+static hipError_t reset_counters(const DevParams& p, hipStream_t s) {
+  hipLaunchKernelGGL(k_reset_state, dim3(1), dim3(kWG), 0, s, p.counters, p.tw_all, int64_t(0));
+  return hipGetLastError();
+}
+
 hipError_t launch_decode_per_op(const DevParams& p, int wbf16, int pos0, int n, int head_wgs,
                                 hipStream_t s) {
+  const hipError_t e0 = reset_counters(p, s);
+  if (e0 != hipSuccess) return e0;
   return dispatch(wbf16, chunks_per_lane(p, wbf16), [&](auto wt, auto cpl) {
     using WT = decltype(wt);
     for (int i = 0; i < n; ++i) {
@@ -1604,6 +1864,8 @@ hipError_t launch_prefill_per_op(const DevParams& p, int wbf16, int pos0, const 
   q.exit_layer = 0;
   q.force_tok = d_tokens;
   q.force_exit = nullptr;
+  const hipError_t e0 = reset_counters(p, s);
+  if (e0 != hipSuccess) return e0;
   return dispatch(wbf16, chunks_per_lane(p, wbf16), [&](auto wt, auto cpl) {
     using WT = decltype(wt);
     for (int i = 0; i < n; ++i) {
@@ -1617,8 +1879,9 @@ hipError_t launch_prefill_per_op(const DevParams& p, int wbf16, int pos0, const 
 
 hipError_t launch_head_eval(const DevParams& p, int wbf16, const float* d_x, int readout, int head_wgs,
                             hipStream_t s) {
-  hipLaunchKernelGGL(k_copy_vec, dim3(8), dim3(kWG), 0, s, p.h, d_x, p.H);
+  hipLaunchKernelGGL(k_tag_vec, dim3(8), dim3(kWG), 0, s, p.h, d_x, p.H);
   hipError_t e = hipGetLastError();
+  if (e == hipSuccess) e = reset_counters(p, s);
   if (e != hipSuccess) return e;
   return dispatch(wbf16, chunks_per_lane(p, wbf16), [&](auto wt, auto cpl) {
     using WT = decltype(wt);
@@ -1655,7 +1918,7 @@ static hipError_t persistent(const PersistentLaunch& L, int pos0, int n, int pre
   hipError_t e = hipMemcpyToSymbolAsync(HIP_SYMBOL(c_params), L.params_host, sizeof(DevParams),
                                         sizeof(DevParams) * L.slot, hipMemcpyHostToDevice, L.stream);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_reset_barrier, dim3(1), dim3(64), 0, L.stream, p.counters);
+  hipLaunchKernelGGL(k_reset_state, dim3(16), dim3(kWG), 0, L.stream, p.counters, p.tw_all, p.tw_words);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   int slot = L.slot;
   void* args[] = {&slot, &pos0, &n, &prefill};
