@@ -50,7 +50,7 @@ struct ee_ctx {
   int64_t tw_words = 0;
   uint64_t *d_h = nullptr, *d_hexit = nullptr, *d_z = nullptr, *d_q = nullptr, *d_o = nullptr,
            *d_a = nullptr, *d_kvnew = nullptr, *d_dec = nullptr;
-  float* d_attn_part = nullptr;
+  uint64_t* d_attn_part = nullptr;  // tagged, inside d_tw
   int max_splits = 0;
   float* d_head_part = nullptr;
   int max_parts = 0;
@@ -563,23 +563,25 @@ int ee_create(const ee_config* cfg, void* hip_stream, ee_ctx** out) {
         (he = hipMemcpy(c->d_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
       return bail(hip_fail(c, he, "hipMemcpy rope tables"));
   }
+  c->max_splits = (g.max_seq + ee::kAttnSplit - 1) / ee::kAttnSplit;
   {
-    const int64_t sizes[8] = {int64_t(H), int64_t(H), int64_t(H), int64_t(A * D), int64_t(A * D),
-                              int64_t(F), int64_t(2 * K * D), 8};
-    uint64_t** ptrs[8] = {&c->d_h, &c->d_hexit, &c->d_z, &c->d_q, &c->d_o, &c->d_a, &c->d_kvnew, &c->d_dec};
+    const int64_t pairs = ((A / K) + 1) / 2;
+    const int64_t sizes[9] = {int64_t(H), int64_t(H), int64_t(H), int64_t(A * D), int64_t(A * D),
+                              int64_t(F), int64_t(2 * K * D), 8,
+                              int64_t(K) * pairs * c->max_splits * int64_t(2 * D + 4)};
+    uint64_t** ptrs[9] = {&c->d_h, &c->d_hexit, &c->d_z, &c->d_q, &c->d_o, &c->d_a, &c->d_kvnew, &c->d_dec,
+                          &c->d_attn_part};
     int64_t total = 0;
-    for (int i = 0; i < 8; ++i) total += (sizes[i] + 31) & ~int64_t(31);  // 256-byte aligned parts
+    for (int i = 0; i < 9; ++i) total += (sizes[i] + 31) & ~int64_t(31);  // 256-byte aligned parts
     if ((r = dalloc(c, &c->d_tw, total * 8)) || (r = dalloc(c, &c->d_x, H * 4))) return bail(r);
     c->tw_words = total;
     int64_t off = 0;
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < 9; ++i) {
       *ptrs[i] = c->d_tw + off;
       off += (sizes[i] + 31) & ~int64_t(31);
     }
     if ((he = hipMemset(c->d_tw, 0, total * 8)) != hipSuccess) return bail(hip_fail(c, he, "hipMemset"));
   }
-  c->max_splits = (g.max_seq + ee::kAttnSplit - 1) / ee::kAttnSplit;
-  if ((r = dalloc(c, &c->d_attn_part, K * c->max_splits * (A / K) * (D + 2) * 4))) return bail(r);
   if ((r = dalloc(c, &c->d_counters, sizeof(ee::Counters)))) return bail(r);
   if ((r = dalloc(c, &c->d_ctl, sizeof(ee::StepCtl)))) return bail(r);
 
@@ -912,7 +914,7 @@ void ee_destroy(ee_ctx* c) {
   if (c->h_block_table) (void)hipHostFree(c->h_block_table);
   dfree(c->d_cos); dfree(c->d_sin);
   dfree(c->d_tw);
-  dfree(c->d_x); dfree(c->d_attn_part); dfree(c->d_head_part); dfree(c->d_counters); dfree(c->d_ctl);
+  dfree(c->d_x); dfree(c->d_head_part); dfree(c->d_counters); dfree(c->d_ctl);
   dfree(c->d_ring_tok); dfree(c->d_ring_exit); dfree(c->d_ring_would); dfree(c->d_ring_conf);
   dfree(c->d_force_tok); dfree(c->d_force_exit); dfree(c->d_dbg_r); dfree(c->d_dbg_f);
   dfree(c->d_timeline);

@@ -56,11 +56,12 @@ enum : int32_t { kErrNone = 0, kErrBarrier = 1, kErrToken = 2, kErrWait = 3 };
 // attention splits of a KV head and of the head workgroups; within one
 // persistent launch they only grow (the last arrival is recognised from the
 // number of arrivals expected so far), one kernel per operation resets them.
+// (The persistent kernel merges attention splits without a counter.)
 struct Counters {
   uint32_t group[kBarGroups][64];
   uint32_t top[64];
   uint32_t gen[64];
-  uint32_t attn[16][64];    // per KV head
+  uint32_t attn[64][64];    // per (KV head, query-head pair), one kernel per operation
   uint32_t head[64];
 };
 
@@ -98,7 +99,7 @@ struct DevParams {
   uint64_t* dec;                // [4] exited, token, readout confidence, gate decision
   uint64_t* tw_all;             // all of the above, one block of tw_words words
   int64_t tw_words;
-  float* attn_part;             // [K][max_splits][G][D] weighted V, then [K][max_splits][G][2] (max, sum)
+  uint64_t* attn_part;          // tagged attention partials [K][(G+1)/2][max_splits][2D + 4]
   int max_splits;
   float* head_part;             // [max_parts][4]
   int max_parts;

@@ -606,28 +606,34 @@ __device__ void phase_qkv(const DevParams& p, int l, int pos, int step, int wg, 
 
 // ---------------------------------------------------------------------------
 // phase: decode attention over positions 0..pos, grouped-query. Workgroup
-// item = (kv head, split of kAttnSplit positions); wave w of the item takes
-// kPosPerWave positions. Lane (sub, dl) of a wave holds 16-byte chunk dl of
-// K and V rows sub + PPW k (LPP lanes per row, PPW rows per load, RPL rows
-// per lane): a row's dot product with q is summed over its LPP lanes with
-// DPP, the softmax statistics over the wave's rows stay in registers, and
-// the weighted V rows are summed over the PPW row groups. The waves merge in
-// LDS; with one split the item writes o directly, otherwise it writes a
-// partial (max, sum of exp, weighted V) and the last split of the kv head to
-// finish merges all splits in index order from LDS.
+// item = (kv head, pair of the query heads sharing it, split of kAttnSplit
+// positions); wave w of the item takes kPosPerWave positions. Lane (sub, dl)
+// of a wave holds 16-byte chunk dl of K and V rows sub + PPW k (LPP lanes per
+// row, PPW rows per load, RPL rows per lane): a row's dot product with q is
+// summed over its LPP lanes with DPP, the softmax statistics over the wave's
+// rows stay in registers, and the weighted V rows are summed over the PPW row
+// groups. The waves merge in LDS; with one split the item writes o directly,
+// otherwise it publishes a partial (weighted V, max, sum of exp) as tagged
+// words and the workgroup of the last split merges the others into o as they
+// land (one kernel per operation: the last split to arrive merges). A
+// workgroup runs its items in increasing order, so a merger only waits for
+// items of lower index, which never wait for it. Splitting the query
+// heads into pairs spreads the work over three times as many workgroups and
+// keeps each partial small.
 //
 // Latency: every K and V row of a lane is loaded with independent loads. The
 // rows of positions before pos were written in earlier steps, so the
-// workgroup issues them (and the page-table lookups) before it waits on the
-// barrier that ends the projection phase; only the row of position pos,
-// written by that phase, is loaded after it.
+// workgroup issues them (and the page-table lookups) before it waits for its
+// input; only the row of position pos, written by the projection phase, is
+// read after it (from its tagged copy).
 // ---------------------------------------------------------------------------
-__host__ __device__ inline int attn_wave_floats(int G, int D) {
-  return 2 * kPosPerWave + G * D + 2 * G;  // offsets | weighted V | m, l
+__host__ __device__ inline int attn_nsplit(int pos) { return (pos + kAttnSplit) / kAttnSplit; }
+__host__ __device__ inline int attn_pairs(int G) { return (G + 1) >> 1; }
+__host__ __device__ inline int attn_wave_floats(int D) {
+  return 2 * kPosPerWave + 2 * D + 4;  // offsets | weighted V of 2 heads | m0 m1 l0 l1
 }
-__host__ __device__ inline int attn_lds_floats(int G, int D) {
-  return G * D + kWaves * attn_wave_floats(G, D);
-}
+__host__ __device__ inline int attn_lds_floats(int D) { return 2 * D + kWaves * attn_wave_floats(D); }
+__host__ __device__ inline int attn_rec_words(int D) { return 2 * D + 4; }  // partial record
 
 // ---------------------------------------------------------------------------
 // LDS layout: xs [vec] | red [64] (block sums, per-wave partial rows)
@@ -637,10 +643,8 @@ __host__ __device__ inline int lds_vec_floats(const DevParams& p) {
   if (p.F > v) v = p.F;
   if (p.A * p.D > v) v = p.A * p.D;
   if (kWG * 4 > v) v = kWG * 4;
-  const int am = attn_lds_floats(p.G, p.D);
+  const int am = attn_lds_floats(p.D);
   if (am > v) v = am;
-  const int mt = 3 * p.max_splits * p.G + p.G;  // merge tables of the last split
-  if (mt > v) v = mt;
   return (v + 63) & ~63;
 }
 
@@ -688,13 +692,14 @@ struct AttnTask {
   bool has_new;
 
   __device__ __forceinline__ static int64_t* offw(const DevParams& p, float* lds) {
-    return reinterpret_cast<int64_t*>(lds + p.G * p.D + wave_id() * attn_wave_floats(p.G, p.D));
+    return reinterpret_cast<int64_t*>(lds + 2 * p.D + wave_id() * attn_wave_floats(p.D));
   }
   // cache offsets of the wave's positions (up to pos) of item it, into LDS
   __device__ __forceinline__ void offsets(const DevParams& p, int l, int pos, int it, int nsplit,
                                           float* lds) {
     const int lane = threadIdx.x & 63;
-    const int kvh = it / nsplit, sp = it - kvh * nsplit;
+    const int per_kvh = attn_pairs(p.G) * nsplit;
+    const int kvh = it / per_kvh, sp = (it - kvh * per_kvh) % nsplit;
     const int ws0 = sp * kAttnSplit + wave_id() * kPosPerWave;
     if (lane < kPosPerWave && ws0 + lane <= pos) offw(p, lds)[lane] = kv_offset(p, l, ws0 + lane, kvh);
     __builtin_amdgcn_wave_barrier();
@@ -723,15 +728,17 @@ struct AttnTask {
     nold = 0;
     has_new = false;
   }
-  // Before the barrier: offsets and the rows of positions < pos of the
-  // workgroup's first item.
+  // Before the input is ready: offsets and the rows of positions < pos of
+  // the workgroup's first item (item it runs on workgroup nwg - 1 - it: the
+  // last workgroups, which own no rows of the projections around attention).
   template <int LPP>
-  __device__ __forceinline__ void prefetch(const DevParams& p, int l, int pos, int wg, float* lds) {
+  __device__ __forceinline__ void prefetch(const DevParams& p, int l, int pos, int wg, int nwg, float* lds) {
     clear();
-    const int nsplit = (pos + kAttnSplit) / kAttnSplit;
-    if (wg >= p.K * nsplit) return;
-    const int ws0 = (wg % nsplit) * kAttnSplit + wave_id() * kPosPerWave;
-    offsets(p, l, pos, wg, nsplit, lds);
+    const int nsplit = attn_nsplit(pos);
+    const int it = nwg - 1 - wg;
+    if (it >= p.K * attn_pairs(p.G) * nsplit) return;
+    const int ws0 = (it % nsplit) * kAttnSplit + wave_id() * kPosPerWave;
+    offsets(p, l, pos, it, nsplit, lds);
     nold = max(0, min(kPosPerWave, pos - ws0));
     has_new = pos >= ws0 && pos < ws0 + kPosPerWave;
     load_old<LPP>(p, offw(p, lds), nold);
@@ -754,15 +761,24 @@ struct AttnTask {
   }
   // the packed chunk of row slot k of this lane (the new row replaces the
   // slot it falls in); a select of values, never a store to a computed slot
+  // (both operands are pinned to registers first: a select between two
+  // members would otherwise become a load through a selected address, which
+  // puts the whole task in private memory)
   template <int LPP>
-  __device__ __forceinline__ uint4 krow(int k, int sub) const {
+  __device__ __forceinline__ uint4 krow(int k, int sub) {
     constexpr int PPW = 64 / LPP;
-    return (has_new && k == nold / PPW && sub == nold % PPW) ? knew : kr[k];
+    uint4 a = kr[k], b = knew;
+    keep_packed(a);
+    keep_packed(b);
+    return (has_new && k == nold / PPW && sub == nold % PPW) ? b : a;
   }
   template <int LPP>
-  __device__ __forceinline__ uint4 vrow(int k, int sub) const {
+  __device__ __forceinline__ uint4 vrow(int k, int sub) {
     constexpr int PPW = 64 / LPP;
-    return (has_new && k == nold / PPW && sub == nold % PPW) ? vnew : vr[k];
+    uint4 a = vr[k], b = vnew;
+    keep_packed(a);
+    keep_packed(b);
+    return (has_new && k == nold / PPW && sub == nold % PPW) ? b : a;
   }
 };
 
@@ -772,224 +788,220 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
   constexpr int N = Elem<WT>::N;
   constexpr int PPW = 64 / LPP, RPL = kPosPerWave / PPW;
   const int T = pos + 1;
-  const int nsplit = (T + kAttnSplit - 1) / kAttnSplit;
-  const int G = p.G, D = p.D;
+  const int nsplit = attn_nsplit(pos);
+  const int G = p.G, D = p.D, GP = attn_pairs(G);
   const int wave = wave_id(), lane = threadIdx.x & 63;
   const int sub = lane / LPP, dl = lane - sub * LPP;
-  float* qs = lds;  // [G][D] q (unscaled)
-  float* wb = lds + G * D + wave * attn_wave_floats(G, D);
-  float* accw = wb + 2 * kPosPerWave;  // [G][D]
-  float* mlw = accw + G * D;           // [G] m, [G] l
+  const int kvh = it / (GP * nsplit), rem = it - kvh * GP * nsplit;
+  const int gp = rem / nsplit, sp = rem - gp * nsplit;
+  const int g0 = 2 * gp, g1 = min(g0 + 1, G - 1);  // g1 == g0: odd G, last pair
+  const int WF = attn_wave_floats(D);
+  float* qs = lds;  // [2][D] q of heads g0, g1 (unscaled)
+  float* wb = lds + 2 * D + wave * WF;
+  float* accw = wb + 2 * kPosPerWave;  // [2][D]
+  float* mlw = accw + 2 * D;           // m0 m1 l0 l1
   __shared__ int last_flag;
 
-  const int kvh = it / nsplit, sp = it - kvh * nsplit;
   const int ws0 = sp * kAttnSplit + wave * kPosPerWave;
   const int wn = max(0, min(kPosPerWave, T - ws0));  // positions of this wave
+  const int tid = threadIdx.x;
   __syncthreads();
-  tw_stage<kMaxGroup * kMaxHeadDim / 2 / kWG>(p, p.q + kvh * G * D, G * D, sy.tin, sy.poll, qs);
+  if (tid < 2 * D)
+    qs[tid] = tw_val(tw_wait(p, p.q + (kvh * G + (tid < D ? g0 : g1)) * D + (tid < D ? tid : tid - D),
+                             sy.tin, sy.poll));
   t.template load_new<LPP>(p, kvh, sy);
   __syncthreads();
 
   if (wn > 0) {
-    // Two query heads per pass. Loops over query heads stay rolled: the
-    // phase runs once per layer, and a fully unrolled body is bound by
-    // instruction fetch rather than arithmetic.
-#pragma nounroll
-    for (int g0 = 0; g0 < G; g0 += 2) {
-      const int g1 = min(g0 + 1, G - 1);
-      float qa[N], qb[N];
+    float qa[N], qb[N];
+#pragma unroll
+    for (int e = 0; e < N; ++e) {
+      qa[e] = qs[dl * N + e];
+      qb[e] = qs[D + dl * N + e];
+    }
+    float sa[RPL], sb[RPL];
+    float ma = -INFINITY, mb = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < RPL; ++k) {
+      uint4 kc = t.template krow<LPP>(k, sub);
+      keep_packed(kc);
+      float kf[N];
+      Elem<WT>::unpack(kc, kf);
+      float x = 0.f, y = 0.f;
 #pragma unroll
       for (int e = 0; e < N; ++e) {
-        qa[e] = qs[g0 * D + dl * N + e];
-        qb[e] = qs[g1 * D + dl * N + e];
+        x = fmaf(qa[e], kf[e], x);
+        y = fmaf(qb[e], kf[e], y);
       }
-      float sa[RPL], sb[RPL];
-      float ma = -INFINITY, mb = -INFINITY;
+      const bool valid = sub + PPW * k < wn;
+      sa[k] = valid ? group_sum(x, LPP == 16) * p.attn_scale : -INFINITY;
+      sb[k] = valid ? group_sum(y, LPP == 16) * p.attn_scale : -INFINITY;
+      ma = fmaxf(ma, sa[k]);
+      mb = fmaxf(mb, sb[k]);
+    }
+    ma = groups_max<LPP>(ma);
+    mb = groups_max<LPP>(mb);
+    float la = 0.f, lb = 0.f;
 #pragma unroll
-      for (int k = 0; k < RPL; ++k) {
-        uint4 kc = t.template krow<LPP>(k, sub);
-        keep_packed(kc);
-        float kf[N];
-        Elem<WT>::unpack(kc, kf);
-        float x = 0.f, y = 0.f;
+    for (int k = 0; k < RPL; ++k) {
+      sa[k] = expf(sa[k] - ma);  // exp(-inf) = 0 for rows past the wave's end
+      sb[k] = expf(sb[k] - mb);
+      la += sa[k];
+      lb += sb[k];
+    }
+    la = groups_sum<LPP>(la);
+    lb = groups_sum<LPP>(lb);
+    float aa[N], ab[N];
 #pragma unroll
-        for (int e = 0; e < N; ++e) {
-          x = fmaf(qa[e], kf[e], x);
-          y = fmaf(qb[e], kf[e], y);
-        }
-        const bool valid = sub + PPW * k < wn;
-        sa[k] = valid ? group_sum(x, LPP == 16) * p.attn_scale : -INFINITY;
-        sb[k] = valid ? group_sum(y, LPP == 16) * p.attn_scale : -INFINITY;
-        ma = fmaxf(ma, sa[k]);
-        mb = fmaxf(mb, sb[k]);
+    for (int e = 0; e < N; ++e) aa[e] = ab[e] = 0.f;
+#pragma unroll
+    for (int k = 0; k < RPL; ++k) {
+      uint4 vc = t.template vrow<LPP>(k, sub);
+      keep_packed(vc);
+      float vf[N];
+      Elem<WT>::unpack(vc, vf);
+#pragma unroll
+      for (int e = 0; e < N; ++e) {
+        aa[e] = fmaf(sa[k], vf[e], aa[e]);
+        ab[e] = fmaf(sb[k], vf[e], ab[e]);
       }
-      ma = groups_max<LPP>(ma);
-      mb = groups_max<LPP>(mb);
-      float la = 0.f, lb = 0.f;
+    }
 #pragma unroll
-      for (int k = 0; k < RPL; ++k) {
-        sa[k] = expf(sa[k] - ma);  // exp(-inf) = 0 for rows past the wave's end
-        sb[k] = expf(sb[k] - mb);
-        la += sa[k];
-        lb += sb[k];
+    for (int off = LPP; off < 64; off <<= 1) {
+#pragma unroll
+      for (int e = 0; e < N; ++e) {
+        aa[e] += __shfl_xor(aa[e], off, 64);
+        ab[e] += __shfl_xor(ab[e], off, 64);
       }
-      la = groups_sum<LPP>(la);
-      lb = groups_sum<LPP>(lb);
-      float aa[N], ab[N];
+    }
+    if (sub == 0) {
 #pragma unroll
-      for (int e = 0; e < N; ++e) aa[e] = ab[e] = 0.f;
-#pragma unroll
-      for (int k = 0; k < RPL; ++k) {
-        uint4 vc = t.template vrow<LPP>(k, sub);
-        keep_packed(vc);
-        float vf[N];
-        Elem<WT>::unpack(vc, vf);
-#pragma unroll
-        for (int e = 0; e < N; ++e) {
-          aa[e] = fmaf(sa[k], vf[e], aa[e]);
-          ab[e] = fmaf(sb[k], vf[e], ab[e]);
-        }
+      for (int e = 0; e < N; ++e) {
+        accw[dl * N + e] = aa[e];
+        accw[D + dl * N + e] = ab[e];
       }
-#pragma unroll
-      for (int off = LPP; off < 64; off <<= 1) {
-#pragma unroll
-        for (int e = 0; e < N; ++e) {
-          aa[e] += __shfl_xor(aa[e], off, 64);
-          ab[e] += __shfl_xor(ab[e], off, 64);
-        }
-      }
-      if (sub == 0) {
-#pragma unroll
-        for (int e = 0; e < N; ++e) {
-          accw[g0 * D + dl * N + e] = aa[e];
-          accw[g1 * D + dl * N + e] = ab[e];  // g1 == g0 writes the same value
-        }
-      }
-      if (lane == 0) {
-        mlw[g0] = ma;
-        mlw[G + g0] = la;
-        mlw[g1] = mb;
-        mlw[G + g1] = lb;
-      }
+    }
+    if (lane == 0) {
+      mlw[0] = ma;
+      mlw[1] = mb;
+      mlw[2] = la;
+      mlw[3] = lb;
     }
   }
   __syncthreads();
-  // merge the waves of this item (fixed order)
+  // merge the waves of this item (fixed order): thread tid owns element
+  // e = tid of [2][D] (head g0 + e / D, dimension e % D)
+  const bool act = tid < 2 * D;
+  const int hg = act ? tid / D : 0, dd = tid - hg * D;
+  const bool dup = hg == 1 && g1 == g0;  // second head of an odd last pair
   const int nw = min(kWaves, (T - sp * kAttnSplit + kPosPerWave - 1) / kPosPerWave);
-  const int64_t kvrec = static_cast<int64_t>(kvh) * p.max_splits;
-  float* pacc = p.attn_part;                                           // [K][S][G][D]
-  float* pml = p.attn_part + static_cast<int64_t>(p.K) * p.max_splits * G * D;  // [K][S][G][2]
-  const float* base0 = lds + G * D;
-  const int WF = attn_wave_floats(G, D);
-  for (int idx = threadIdx.x; idx < G * D; idx += kWG) {
-    const int g = idx / D;
-    float mw[kWaves], aw[kWaves], lw[kWaves];
+  float M = -INFINITY, den = 0.f, num = 0.f;
+  {
+    float mw[kWaves];
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) mw[w] = w < nw ? lds[2 * D + w * WF + 2 * kPosPerWave + 2 * D + hg] : -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, mw[w]);
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
-      const float* wb2 = base0 + w * WF + 2 * kPosPerWave;
-      mw[w] = w < nw ? wb2[G * D + g] : -INFINITY;
-      lw[w] = w < nw ? wb2[G * D + G + g] : 0.f;
-      aw[w] = w < nw ? wb2[idx] : 0.f;
-    }
-    float M = mw[0];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) M = fmaxf(M, mw[w]);
-    float den = 0.f, num = 0.f;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      const float f = w < nw ? expf(mw[w] - M) : 0.f;
-      den = fmaf(f, lw[w], den);
-      num = fmaf(f, aw[w], num);
-    }
-    if (nsplit == 1) {
-      tw_store(p.o + kvh * G * D + idx, num / den, sy.tout);
-    } else {
-      st_coh(pacc + (kvrec + sp) * G * D + idx, num);
-      if (idx - g * D == 0) st_coh2(pml + ((kvrec + sp) * G + g) * 2, M, den);
-    }
-  }
-  if (nsplit == 1) return;
-  // the last split of this kv head to finish merges all splits into o
-  wait_stores();
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const uint32_t old = __hip_atomic_fetch_add(&p.counters->attn[kvh][0], 1u, __ATOMIC_RELAXED,
-                                                __HIP_MEMORY_SCOPE_AGENT);
-    last_flag = (old == sy.cbase + static_cast<uint32_t>(nsplit - 1));
-  }
-  __syncthreads();
-  if (!last_flag) return;
-  // One round trip for up to kSC splits: each thread issues the loads of its
-  // output elements for a batch of splits, then the (max, sum) table of all
-  // splits is staged; the split weights exp(m_s - M) and 1 / sum are formed
-  // once per query head.
-  constexpr int kIdx = kMaxGroup * kMaxHeadDim / 2 / kWG;  // G D <= 1024 (rows <= 256 bytes)
-  constexpr int kSC = 8;
-  const float* accb = pacc + kvrec * G * D;
-  float* mll = lds;                  // [nsplit][G][2]
-  float* fl = lds + 2 * nsplit * G;  // [nsplit][G] split weights, then [G] 1 / sum
-  float num[kIdx], av[kIdx][kSC];
-#pragma unroll
-  for (int k = 0; k < kIdx; ++k) {
-    num[k] = 0.f;
-    const int idx = static_cast<int>(threadIdx.x) + k * kWG;
-#pragma unroll
-    for (int s = 0; s < kSC; ++s)
-      av[k][s] = (idx < G * D && s < nsplit) ? ld_coh(accb + s * G * D + idx) : 0.f;
-  }
-  stage_coh(pml + kvrec * G * 2, 2 * nsplit * G, mll);
-  __syncthreads();
-  if (static_cast<int>(threadIdx.x) < G) {
-    const int g = threadIdx.x;
-    float M = -INFINITY;
-    for (int s = 0; s < nsplit; ++s) M = fmaxf(M, mll[(s * G + g) * 2]);
-    float den = 0.f;
-    for (int s = 0; s < nsplit; ++s) {
-      const float f = expf(mll[(s * G + g) * 2] - M);
-      fl[s * G + g] = f;
-      den = fmaf(f, mll[(s * G + g) * 2 + 1], den);
-    }
-    fl[nsplit * G + g] = 1.f / den;
-  }
-  __syncthreads();
-  for (int s0 = 0; s0 < nsplit; s0 += kSC) {
-    if (s0 > 0) {
-#pragma unroll
-      for (int k = 0; k < kIdx; ++k) {
-        const int idx = static_cast<int>(threadIdx.x) + k * kWG;
-#pragma unroll
-        for (int s = 0; s < kSC; ++s)
-          av[k][s] = (idx < G * D && s0 + s < nsplit) ? ld_coh(accb + (s0 + s) * G * D + idx) : 0.f;
+      if (w < nw) {
+        const float* wb2 = lds + 2 * D + w * WF + 2 * kPosPerWave;
+        const float f = expf(mw[w] - M);
+        den = fmaf(f, wb2[2 * D + 2 + hg], den);
+        num = fmaf(f, act ? wb2[tid] : 0.f, num);
       }
     }
-#pragma unroll
-    for (int k = 0; k < kIdx; ++k) {
-      const int idx = min(static_cast<int>(threadIdx.x) + k * kWG, G * D - 1);
-      const int g = idx / D;
-#pragma unroll
-      for (int s = 0; s < kSC; ++s)
-        if (s0 + s < nsplit) num[k] = fmaf(fl[(s0 + s) * G + g], av[k][s], num[k]);
+  }
+  uint64_t* outp = p.o + (kvh * G + g0 + hg) * D + dd;
+  if (nsplit == 1) {
+    if (act && !dup) tw_store(outp, num / den, sy.tout);
+    return;
+  }
+  // partial records, tagged: [K][GP][max_splits][2D weighted V | m0 m1 | l0 l1]
+  const int RS = attn_rec_words(D);
+  uint64_t* recs = p.attn_part + (static_cast<int64_t>(kvh) * GP + gp) * p.max_splits * RS;
+  const bool merger = sy.poll && sp == nsplit - 1;
+  if (!merger) {
+    uint64_t* r = recs + static_cast<int64_t>(sp) * RS;
+    if (act) tw_store(r + tid, num, sy.tout);
+    if (act && dd == 0) {
+      tw_store(r + 2 * D + hg, M, sy.tout);
+      tw_store(r + 2 * D + 2 + hg, den, sy.tout);
+    }
+    if (sy.poll) return;
+    wait_stores();
+    __syncthreads();
+    if (tid == 0) {
+      const uint32_t old = __hip_atomic_fetch_add(&p.counters->attn[kvh * GP + gp][0], 1u,
+                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      last_flag = (old == static_cast<uint32_t>(nsplit - 1));
+    }
+    __syncthreads();
+    if (!last_flag) return;
+  }
+  // Merge in chunks of splits staged into LDS, in split order: per head a
+  // running max and sum (held by the head's first thread), per element a
+  // running weighted V. The merger (the last split) writes its own record
+  // into its slot instead of reading it back, so both programs do the same
+  // arithmetic in the same order.
+  float Mr = -INFINITY, Dr = 0.f, Nr = 0.f;
+  const int cap = max(1, (lds_vec_floats(p) - 8) / (RS + 2));
+  float* rl = lds;                 // [cap][RS]
+  float* wts = lds + cap * RS;     // [cap][2] split weights
+  float* hsc = wts + 2 * cap;      // [2] rescale of the running values, then [2] 1 / sum
+  for (int c0 = 0; c0 < nsplit; c0 += cap) {
+    const int ns = min(cap, nsplit - c0);
+    const bool own = merger && c0 + ns == nsplit;  // this chunk holds the merger's split
+    __syncthreads();  // LDS may still be read (wave records, previous chunk)
+    tw_stage<12>(p, recs + static_cast<int64_t>(c0) * RS, (ns - (own ? 1 : 0)) * RS, sy.tout, sy.poll, rl);
+    if (own) {
+      float* r = rl + (ns - 1) * RS;
+      if (act) r[tid] = num;
+      if (act && dd == 0) {
+        r[2 * D + hg] = M;
+        r[2 * D + 2 + hg] = den;
+      }
+    }
+    __syncthreads();
+    if (act && dd == 0) {
+      float cm = Mr;
+      for (int s2 = 0; s2 < ns; ++s2) cm = fmaxf(cm, rl[s2 * RS + 2 * D + hg]);
+      const float sc = expf(Mr - cm);  // 0 while nothing has been merged yet
+      float dn = Dr * sc;
+      for (int s2 = 0; s2 < ns; ++s2) {
+        const float f = expf(rl[s2 * RS + 2 * D + hg] - cm);
+        wts[s2 * 2 + hg] = f;
+        dn = fmaf(f, rl[s2 * RS + 2 * D + 2 + hg], dn);
+      }
+      hsc[hg] = sc;
+      Mr = cm;
+      Dr = dn;
+    }
+    __syncthreads();
+    if (act) {
+      Nr *= hsc[hg];
+      for (int s2 = 0; s2 < ns; ++s2) Nr = fmaf(wts[s2 * 2 + hg], rl[s2 * RS + tid], Nr);
     }
   }
-#pragma unroll
-  for (int k = 0; k < kIdx; ++k) {
-    const int idx = static_cast<int>(threadIdx.x) + k * kWG;
-    if (idx < G * D) tw_store(p.o + kvh * G * D + idx, num[k] * fl[nsplit * G + idx / D], sy.tout);
-  }
-  if (!sy.poll && threadIdx.x == 0)
-    __hip_atomic_store(&p.counters->attn[kvh][0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  if (act && dd == 0) hsc[2 + hg] = 1.f / Dr;
+  __syncthreads();
+  if (act && !dup) tw_store(outp, Nr * hsc[2 + hg], sy.tout);
+  if (!sy.poll && tid == 0)
+    __hip_atomic_store(&p.counters->attn[kvh * GP + gp][0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // The first item of the workgroup uses the rows t prefetched; further items
 // (more than one per workgroup only past nwg * kAttnSplit / K positions) load
-// all of theirs after the barrier.
+// theirs when they start.
 template <typename WT, int LPP>
 __device__ __forceinline__ void phase_attn(const DevParams& p, int l, int pos, int wg, int nwg,
                                            float* lds, AttnTask<WT>& t, const Sync& sy) {
-  const int nsplit = (pos + kAttnSplit) / kAttnSplit;
-  const int items = p.K * nsplit;
-  for (int it = wg; it < items; it += nwg) {
-    if (it != wg) {
+  const int nsplit = attn_nsplit(pos);
+  const int items = p.K * attn_pairs(p.G) * nsplit;
+  const int first = nwg - 1 - wg;
+  for (int it = first; it < items; it += nwg) {
+    if (it != first) {
       __syncthreads();  // offsets of the previous item may still be read
       t.offsets(p, l, pos, it, nsplit, lds);
       const int ws0 = (it % nsplit) * kAttnSplit + wave_id() * kPosPerWave;
@@ -1418,10 +1430,10 @@ __global__ __launch_bounds__(kWG) void k_op(DevParams p, int l, int pos, int ste
   if constexpr (OP == kOpAttn) {
     AttnTask<WT> t;
     if (attn_row_chunks<WT>(p) == 16) {
-      t.template prefetch<16>(p, l, pos, wg, s.xs);
+      t.template prefetch<16>(p, l, pos, wg, nwg, s.xs);
       phase_attn<WT, 16>(p, l, pos, wg, nwg, s.xs, t, sy);
     } else {
-      t.template prefetch<8>(p, l, pos, wg, s.xs);
+      t.template prefetch<8>(p, l, pos, wg, nwg, s.xs);
       phase_attn<WT, 8>(p, l, pos, wg, nwg, s.xs, t, sy);
     }
   }
@@ -1458,7 +1470,7 @@ __global__ __launch_bounds__(kWG) void k_op(DevParams p, int l, int pos, int ste
 static int op_grid(const DevParams& p, int op, int pos, int head_wgs) {
   switch (op) {
     case kOpQkv: return ((p.qkv_rows >> 1) + kWaves - 1) / kWaves;
-    case kOpAttn: return p.K * ((pos + 1 + kAttnSplit - 1) / kAttnSplit);
+    case kOpAttn: return p.K * attn_pairs(p.G) * attn_nsplit(pos);
     case kOpWo:
     case kOpReadout: return (p.H + kWaves - 1) / kWaves;
     case kOpGateUp: return (p.F + kWaves * 4 - 1) / (kWaves * 4);
@@ -1585,7 +1597,6 @@ struct Tags {
   uint32_t h, q, o, a, z, hx;  // latest version of each vector
   uint32_t gate;               // latest gate record (readout head)
   uint32_t tok;                // record holding the next input token
-  uint32_t attn;               // arrivals per KV head on the attention counter
   uint32_t heads;              // head phases run
 };
 
@@ -1626,29 +1637,30 @@ EE_PHASE_FN run_attn(const DevParams& p, int l, int pos, float* smem, Tags& tg) 
   // may still be reading as the projection phase's input
   __syncthreads();
   const uint32_t E = ++tg.ep;
-  const Sync sy{true, tg.q, 0u, E, tg.attn};
+  const Sync sy{true, tg.q, 0u, E, 0u};
   if (attn_row_chunks<WT>(p) == 16) {
-    t.template prefetch<16>(p, l, pos, wg, smem);
+    t.template prefetch<16>(p, l, pos, wg, gridDim.x, smem);
     tl_mark(p, 2 * E);
     phase_attn<WT, 16>(p, l, pos, wg, gridDim.x, smem, t, sy);
   } else {
-    t.template prefetch<8>(p, l, pos, wg, smem);
+    t.template prefetch<8>(p, l, pos, wg, gridDim.x, smem);
     tl_mark(p, 2 * E);
     phase_attn<WT, 8>(p, l, pos, wg, gridDim.x, smem, t, sy);
   }
   tl_mark(p, 2 * E + 1);
   tg.o = E;
-  // a single split writes o itself and never arrives on the counter
-  const int nsplit = (pos + kAttnSplit) / kAttnSplit;
-  if (nsplit > 1) tg.attn += static_cast<uint32_t>(nsplit);
 }
 
-EE_PHASE_FN run_wo(const DevParams& p, int l, float* smem, Tags& tg) {
+// The gate/up tiles are requested here too, before the wait for the
+// attention output: most workgroups have no attention item and would leave
+// HBM idle while the attention workgroups finish.
+EE_PHASE_FN run_wo(const DevParams& p, int l, float* smem, Tags& tg, GateUpTask<WT, CPL>& gu) {
   const int wg = opaque_wg();
   const Lds s = lds_carve(p, smem);
   const WT* W = static_cast<const WT*>(p.layers[l].wo);
   RowTask<WT, CPL> t;
   t.prefetch(W, p.H, p.A * p.D, wg);
+  gu.prefetch(p, l, wg, gridDim.x);
   const uint32_t E = ++tg.ep;
   tl_mark(p, 2 * E);
   phase_rows<WT, CPL>(p, W, p.H, p.A * p.D, p.o, p.h, nullptr, 1, wg, gridDim.x, s.xs, t,
@@ -1657,11 +1669,9 @@ EE_PHASE_FN run_wo(const DevParams& p, int l, float* smem, Tags& tg) {
   tg.h = E;
 }
 
-EE_PHASE_FN run_gateup(const DevParams& p, int l, float* smem, Tags& tg) {
+EE_PHASE_FN run_gateup(const DevParams& p, int l, float* smem, Tags& tg, GateUpTask<WT, CPL>& t) {
   const int wg = opaque_wg();
   const Lds s = lds_carve(p, smem);
-  GateUpTask<WT, CPL> t;
-  t.prefetch(p, l, wg, gridDim.x);
   const uint32_t E = ++tg.ep;
   tl_mark(p, 2 * E);
   phase_gateup<WT, CPL>(p, l, wg, gridDim.x, s.xs, s.red, t, Sync{true, tg.h, 0u, E, 0u});
@@ -1724,8 +1734,9 @@ __device__ __forceinline__ void run_layer(const DevParams& p, int l, int pos, in
                                           Tags& tg) {
   run_qkv<WT, CPL>(p, l, pos, step, smem, tg);
   run_attn<WT, CPL>(p, l, pos, smem, tg);
-  run_wo<WT, CPL>(p, l, smem, tg);
-  run_gateup<WT, CPL>(p, l, smem, tg);
+  GateUpTask<WT, CPL> gu;
+  run_wo<WT, CPL>(p, l, smem, tg, gu);
+  run_gateup<WT, CPL>(p, l, smem, tg, gu);
   run_down<WT, CPL>(p, l, smem, tg);
 }
 
@@ -1786,7 +1797,7 @@ __global__ __launch_bounds__(kWG) void k_reset_state(Counters* c, uint64_t* tw, 
   const int t = threadIdx.x;
   if (blockIdx.x == 0) {
     if (t < kBarGroups) c->group[t][0] = 0u;
-    if (t < 16) c->attn[t][0] = 0u;
+    if (t < 64) c->attn[t][0] = 0u;
     if (t == 0) {
       c->top[0] = 0u;
       c->gen[0] = 0u;
