@@ -1108,7 +1108,7 @@ __device__ void phase_gateup(const DevParams& p, int l, int wg, int nwg, float* 
 template <typename WT, int CPL>
 struct DownTask {
   RowBlock<WT, kRS, CPL> a, b;
-  float hres;  // residual h[rb + threadIdx.x] of the workgroup's rows (first kWG rows)
+  uint64_t hraw;  // residual word h[rb + threadIdx.x] of the workgroup's rows (first kWG rows)
   __device__ __forceinline__ static Tiling<WT, kRS, CPL> tiling(const DevParams& p, int wg, int nwg) {
     const int nch = p.F / Elem<WT>::N;
     const int longest = (nch + kWaves - 1) / kWaves;
@@ -1117,15 +1117,17 @@ struct DownTask {
                                 nch * wave_id() / kWaves, nch * (wave_id() + 1) / kWaves,
                                 max(1, (longest + 64 * CPL - 1) / (64 * CPL))};
   }
-  // Before the input is ready: the first two tiles, and the residual rows (h
-  // is last written by the output projection, before the gate/up phase).
-  __device__ __forceinline__ void prefetch(const DevParams& p, int l, int wg, int nwg, const Sync& sy) {
+  // Before the input is ready: the residual words (h is last written by the
+  // output projection, before the gate/up phase), then the first two tiles.
+  // Nothing waits here: the residual's tag is checked once a is staged (a
+  // wait now would also wait for the tiles requested after it).
+  __device__ __forceinline__ void prefetch(const DevParams& p, int l, int wg, int nwg) {
     const auto tl = tiling(p, wg, nwg);
     const WT* W = static_cast<const WT*>(p.layers[l].wd);
+    const int r = tl.rb + static_cast<int>(threadIdx.x);
+    hraw = r < tl.re ? ld_coh_u64(p.h + r) : 0ull;
     if (tl.count() > 0) tl.load(a, W, p.F, 0);
     if (tl.count() > 1) tl.load(b, W, p.F, 1);
-    const int r = tl.rb + static_cast<int>(threadIdx.x);
-    hres = r < tl.re ? tw_val(tw_wait(p, p.h + r, sy.tres, sy.poll)) : 0.f;
   }
 };
 
@@ -1137,6 +1139,9 @@ __device__ void phase_down(const DevParams& p, int l, int wg, int nwg, float* xs
   copy_stage<18>(p, p.a, p.F, sy, xs);
   const int wave = wave_id();
   const int tid = threadIdx.x;
+  float hres = 0.f;
+  if (tl.rb + tid < tl.re)
+    hres = tw_val(tw_ok(t.hraw, sy.tres) ? t.hraw : tw_wait(p, p.h + tl.rb + tid, sy.tres, sy.poll));
   uint64_t* h = p.h;
   stream_tiles<WT, kRS, CPL>(static_cast<const WT*>(p.layers[l].wd), p.F, tl, xs, t.a, t.b,
                              [&](int r0, int nr, const float(&acc)[kRS]) {
@@ -1150,7 +1155,7 @@ __device__ void phase_down(const DevParams& p, int l, int wg, int nwg, float* xs
                                if (i >= 0 && i < nr) {
                                  float sum = 0.f;
                                  for (int w = 0; w < kWaves; ++w) sum += red[w * kRS + i];
-                                 tw_store(h + r0 + i, t.hres + sum, sy.tout);
+                                 tw_store(h + r0 + i, hres + sum, sy.tout);
                                } else if (r0 - tl.rb + nr > kWG && tid < nr && r0 - tl.rb + tid >= kWG) {
                                  float sum = 0.f;
                                  for (int w = 0; w < kWaves; ++w) sum += red[w * kRS + tid];
@@ -1450,7 +1455,7 @@ __global__ __launch_bounds__(kWG) void k_op(DevParams p, int l, int pos, int ste
   }
   if constexpr (OP == kOpDown) {
     DownTask<WT, CPL> t;
-    t.prefetch(p, l, wg, nwg, sy);
+    t.prefetch(p, l, wg, nwg);
     phase_down<WT, CPL>(p, l, wg, nwg, s.xs, s.red, t, sy);
   }
   if constexpr (OP == kOpReadout) {
@@ -1685,7 +1690,7 @@ EE_PHASE_FN run_down(const DevParams& p, int l, float* smem, Tags& tg) {
   const uint32_t E = ++tg.ep;
   const Sync sy{true, tg.a, tg.h, E, 0u};
   DownTask<WT, CPL> t;
-  t.prefetch(p, l, wg, gridDim.x, sy);
+  t.prefetch(p, l, wg, gridDim.x);
   tl_mark(p, 2 * E);
   phase_down<WT, CPL>(p, l, wg, gridDim.x, s.xs, s.red, t, sy);
   tl_mark(p, 2 * E + 1);
