@@ -33,7 +33,7 @@ import os
 
 import numpy as np
 
-from .numerics import bf16_bits_to_f64, head_stats, rmsnorm, rope, round_to_storage, silu
+from .numerics import bf16_bits_to_f64, confidence_measures, head_stats, rmsnorm, rope, round_to_storage, silu
 
 
 def _mat(a: np.ndarray, wdtype: str, pool=None) -> np.ndarray:
@@ -54,7 +54,7 @@ def _mat(a: np.ndarray, wdtype: str, pool=None) -> np.ndarray:
 class StepResult:
     token: int                 # emitted token
     exited: bool               # branch taken
-    conf: float                # readout confidence (full head's when ungated)
+    conf: float                # readout confidence under the chosen measure (full head's when ungated)
     would_exit: bool           # gate decision before any forcing
     readout_token: int = -1
     gap_readout: float = math.inf
@@ -65,6 +65,7 @@ class StepResult:
     h_final: np.ndarray = None # residual after layer L (None when exited)
     logits_readout: np.ndarray = None
     logits_full: np.ndarray = None
+    measures: dict = None      # all three measures of the head that set conf
 
 
 class OracleDecoder:
@@ -158,7 +159,9 @@ class OracleDecoder:
 
     # -- decode ----------------------------------------------------------------
     def decode_step(self, token: int, tau: float, exit_layer: int, force_exit: int = -1,
-                    keep_logits: bool = False) -> StepResult:
+                    keep_logits: bool = False, measure: str = "maxprob") -> StepResult:
+        """One gated step. measure selects the confidence the gate compares
+        with tau (maxprob, margin or negentropy); exit iff it exceeds tau."""
         c = self.cfg
         L = c.n_layers
         if not (0 <= exit_layer <= L):
@@ -178,6 +181,8 @@ class OracleDecoder:
         if exit_layer:
             lr = self.readout_logits(h_exit, exit_layer)
             res.readout_token, res.conf, res.gap_readout = head_stats(lr)
+            res.measures = confidence_measures(lr)
+            res.conf = res.measures[measure]
             res.would_exit = bool(np.float32(res.conf) > np.float32(tau))
             res.exited = res.would_exit if force_exit < 0 else bool(force_exit)
             if keep_logits:
@@ -194,6 +199,8 @@ class OracleDecoder:
             res.token = res.full_token
             res.h_final = h
             if not exit_layer:
+                res.measures = confidence_measures(lf)
+                res.conf_full = res.measures[measure]
                 res.conf = res.conf_full
             if keep_logits:
                 res.logits_full = lf
@@ -241,7 +248,7 @@ class OracleDecoder:
         return self.last_prefill_stats[0]
 
     def generate(self, first_token: int, tau: float, exit_layer: int, n: int,
-                 force_tokens=None, force_exit=None, keep_logits=False):
+                 force_tokens=None, force_exit=None, keep_logits=False, measure="maxprob"):
         """n decode steps. Free-running unless force_tokens (input token per
         step) is given; force_exit (per step, -1/0/1) imposes branches."""
         out = []
@@ -250,7 +257,7 @@ class OracleDecoder:
             if force_tokens is not None:
                 tok = int(force_tokens[i])
             fe = -1 if force_exit is None else int(force_exit[i])
-            r = self.decode_step(tok, tau, exit_layer, fe, keep_logits)
+            r = self.decode_step(tok, tau, exit_layer, fe, keep_logits, measure)
             out.append(r)
             tok = r.token
         return out

@@ -62,3 +62,26 @@ def head_stats(logits: np.ndarray):
     conf = 1.0 / float(np.sum(np.exp(logits - m)))
     gap = float(m - np.partition(logits, -2)[-2]) if logits.size > 1 else np.inf
     return j, conf, gap
+
+
+MEASURES = ("maxprob", "margin", "negentropy")
+
+
+def confidence_measures(logits: np.ndarray) -> dict:
+    """The three softmax confidence measures the paper compares (Section 10:
+    probability of the best token, margin between the best and second-best
+    probabilities, negative entropy of the distribution), at temperature one,
+    in fp64:
+      maxprob    = p_(1)
+      margin     = p_(1) - p_(2)            (0 when the two best tie)
+      negentropy = sum_i p_i log p_i        (<= 0; 0 log 0 = 0)
+    """
+    x = np.asarray(logits, dtype=np.float64)
+    p = np.exp(x - x.max())
+    p /= p.sum()
+    top = np.sort(p)[::-1]
+    nz = p[p > 0]
+    return {"maxprob": float(top[0]),
+            "margin": float(top[0] - top[1]) if p.size > 1 else float(top[0]),
+            "negentropy": float(np.sum(nz * np.log(nz)))}
+

@@ -99,6 +99,30 @@ def test_teacher_forced_confidence_independent_of_tau_and_exits_monotone(w):
     assert 0 < len({i for i, r in enumerate(runs[0.5]) if r.exited}) < 32
 
 
+@pytest.mark.parametrize("measure,never,always", [("margin", 1.0, -1e-30), ("negentropy", 0.0, -math.inf)])
+def test_gate_measures(w, measure, never, always):
+    """The gate under the margin and negative-entropy measures (Section 10):
+    the measure's range fixes the thresholds that never / always exit, the
+    gated step's conf is the measure of the readout's logits, and max-prob
+    mode is the default."""
+    toks = seq(24, 5)
+    o = oracle.OracleDecoder(CFG, w, 64)
+    rs = o.generate(o.prefill(seq(P, 1)), math.inf, 2, 24, force_tokens=toks, keep_logits=True,
+                    measure=measure)
+    for r in rs:
+        assert r.conf == oracle.confidence_measures(r.logits_readout)[measure]
+    for tau, expect in ((never, 0), (always, 24)):
+        o = oracle.OracleDecoder(CFG, w, 64)
+        rs2 = o.generate(o.prefill(seq(P, 1)), tau, 2, 24, force_tokens=toks, measure=measure)
+        assert sum(r.exited for r in rs2) == expect
+        assert [r.conf for r in rs2] == [r.conf for r in rs]
+    o = oracle.OracleDecoder(CFG, w, 64)
+    d = o.generate(o.prefill(seq(P, 1)), 0.5, 2, 24, force_tokens=toks)
+    o = oracle.OracleDecoder(CFG, w, 64)
+    m = o.generate(o.prefill(seq(P, 1)), 0.5, 2, 24, force_tokens=toks, measure="maxprob")
+    assert [(r.token, r.exited, r.conf) for r in d] == [(r.token, r.exited, r.conf) for r in m]
+
+
 def test_readout_special_cases(w):
     """Logit lens (W = I, b = 0) at L_e = L equals the full head; a permutation
     readout permutes the residual; an offset of -h zeroes the normalised state,

@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 import torch
 
-from oracle.numerics import bf16_bits_to_f64, head_stats, rmsnorm, rope, round_to_storage, silu
+from oracle.numerics import bf16_bits_to_f64, confidence_measures, head_stats, rmsnorm, rope, round_to_storage, silu
 import synth
 
 
@@ -103,3 +103,42 @@ def test_head_stats_brute_force():
         assert gap == lg[order[0]] - lg[order[1]]
     j, conf, gap = head_stats(np.zeros(4096))
     assert j == 0 and conf == 1.0 / 4096 and gap == 0.0
+
+
+def test_confidence_measures_library_and_closed_forms():
+    """The three confidence measures (Section 10) against library routines and
+    closed forms: negative entropy vs scipy's entropy, the best probability
+    vs the head's own confidence, margins and entropies of two-token and
+    uniform distributions, and ties."""
+    from scipy.special import softmax
+    from scipy.stats import entropy
+    rng = np.random.default_rng(11)
+    for V, scale in ((2, 1.0), (7, 3.0), (1000, 5.0), (151936, 5.0)):
+        x = rng.standard_normal(V) * scale
+        m = confidence_measures(x)
+        p = softmax(x)
+        assert m["maxprob"] == pytest.approx(head_stats(x)[1], rel=1e-12)
+        assert m["negentropy"] == pytest.approx(-entropy(p), rel=1e-10, abs=1e-12)
+        q = np.sort(p)
+        assert m["margin"] == pytest.approx(q[-1] - q[-2], rel=1e-10, abs=1e-15)
+        assert 0.0 <= m["margin"] <= m["maxprob"] <= 1.0
+        assert -math.log(V) - 1e-9 <= m["negentropy"] <= 0.0
+    # two tokens, logit difference d: p = sigmoid(d)
+    for d in (0.0, 0.3, 2.0, 9.0):
+        m = confidence_measures(np.array([d, 0.0]))
+        s = 1.0 / (1.0 + math.exp(-d))
+        assert m["margin"] == pytest.approx(math.tanh(d / 2), abs=1e-14)
+        assert m["negentropy"] == pytest.approx(s * math.log(s) + (1 - s) * math.log(1 - s), abs=1e-14)
+    # uniform: no margin, entropy log V
+    m = confidence_measures(np.full(4096, 1.25))
+    assert m["margin"] == 0.0 and m["maxprob"] == pytest.approx(1 / 4096)
+    assert m["negentropy"] == pytest.approx(-math.log(4096), rel=1e-13)
+    # a tie at the top: zero margin whatever the rest
+    x = rng.standard_normal(500)
+    x[[17, 300]] = x.max() + 1.0
+    assert confidence_measures(x)["margin"] == 0.0
+    # a dominant token: maxprob and margin near 1, entropy near 0 (underflow safe)
+    x = np.zeros(1000)
+    x[5] = 800.0
+    m = confidence_measures(x)
+    assert m["maxprob"] == 1.0 and m["margin"] == 1.0 and m["negentropy"] == 0.0
