@@ -27,6 +27,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "batch-1 decode tokens/sec at exit rate r; achieved HBM GB/s vs peak"
 PEAK_HBM_GBS = 8000.0
+MEASURES = {"maxprob": 0, "margin": 1, "negentropy": 2}  # EE_CONF_* of include/ee.h
 PROMPT = 512
 
 
@@ -98,7 +99,7 @@ def run_condition(e, cfg, tau, exit_layer, prompt, warmup, steps):
     }
 
 
-def cpu_baseline(cfg, w, prompt, tau, exit_layer, seconds):
+def cpu_baseline(cfg, w, prompt, tau, exit_layer, seconds, measure="maxprob"):
     """The CPU oracle (fp64 numpy) on a bounded sample of the same workload."""
     import numpy as np
     import oracle
@@ -117,7 +118,7 @@ def cpu_baseline(cfg, w, prompt, tau, exit_layer, seconds):
     exits = 0
     t = time.perf_counter()
     while True:
-        r = o.decode_step(tok, tau, exit_layer)
+        r = o.decode_step(tok, tau, exit_layer, measure=measure)
         tok = r.token
         exits += r.exited
         n += 1
@@ -145,6 +146,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--confidence", choices=list(MEASURES), default="maxprob",
+                    help="softmax confidence measure the gate compares with tau (Section 10)")
     ap.add_argument("--copy-probe", type=float, default=0.0, metavar="MIB",
                     help="first run one plain elementwise copy of MIB MiB (float32 neg), whose "
                          "profiler counters scale the decode kernel's byte counters")
@@ -182,6 +185,7 @@ def main():
     e = Engine(cfg, max_seq)
     e.ee_load_weights(w)
     e.ee_set_persistent(args.program == "persistent")
+    e.ee_set_confidence_measure(MEASURES[args.confidence])
     log("weights resident on the GPU")
 
     cal = [synth.prompts(cfg, 200 + i, PROMPT) for i in range(args.cal_prompts)]
@@ -221,7 +225,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         t = time.perf_counter()
-        cpu = cpu_baseline(cfg, w, prompt, taus[0.5], Le, args.cpu_seconds)
+        cpu = cpu_baseline(cfg, w, prompt, taus[0.5], Le, args.cpu_seconds, args.confidence)
         log(f"cpu baseline {cpu} ({time.perf_counter() - t:.1f}s incl. setup)")
 
     out = {
@@ -248,6 +252,7 @@ def main():
             "realised_exit_rate": head["realised_exit_rate"],
             "tau": head["tau"],
             "program": args.program,
+            "confidence": args.confidence,
         },
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -59,6 +59,14 @@ enum {
   EE_CAL_MEDIAN = 1     /* tau = median readout confidence (target ignored) */
 };
 
+/* Confidence measures the gate can compare with tau (Section 10 compares
+ * these three softmax measures of the readout's distribution p). */
+enum {
+  EE_CONF_MAXPROB = 0,   /* p of the best token (the default; Section 2) */
+  EE_CONF_MARGIN = 1,    /* best minus second-best probability, in [0, 1) */
+  EE_CONF_NEGENTROPY = 2 /* sum_i p_i log p_i (natural log), in [-log V, 0] */
+};
+
 typedef struct ee_config {
   int32_t n_layers;   /* L */
   int32_t hidden;     /* H, multiple of 8 */
@@ -173,6 +181,13 @@ int ee_calibrate_threshold(ee_ctx* ctx, const int32_t* prompts, const int32_t* p
                            int32_t n_prompts, int32_t n_gen, int32_t exit_layer,
                            int32_t mode, float target, float* out_tau);
 
+/* Select the confidence measure (EE_CONF_*) for the gate (exit iff the
+ * measure exceeds tau), for the conf values decode calls report, for
+ * calibration and for ee_head_eval. All three come from the same single pass
+ * over the vocabulary. Takes effect at the next call; the context starts with
+ * EE_CONF_MAXPROB. Errors: EE_EINVAL (unknown measure). */
+int ee_set_confidence_measure(ee_ctx* ctx, int32_t measure);
+
 /* Replace the offset b (H fp32) of the readout at exit_layer, asynchronously
  * on the context's stream (no sync): later steps enqueued on the stream see
  * it. Errors: EE_EINVAL (no readout at that layer), EE_EHIP. */
@@ -181,7 +196,8 @@ int ee_set_readout_bias(ee_ctx* ctx, int32_t exit_layer, const float* b, int32_t
 /* Evaluate one head on a caller vector x (H fp32, host): layer 0 = the full
  * head (final RMSNorm + unembedding), layer L_e = the readout at L_e followed
  * by the full head. Runs the decode step's head kernel. Outputs (any may be
- * NULL): argmax token, max-probability, logits [V] (host). Test hook. */
+ * NULL): argmax token, confidence under the selected measure, logits [V]
+ * (host). Test hook. */
 int ee_head_eval(ee_ctx* ctx, int32_t readout_layer, const float* x,
                  int32_t* out_token, float* out_conf, float* out_logits);
 

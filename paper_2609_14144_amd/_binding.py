@@ -14,6 +14,7 @@ lib_path = os.path.join(_HERE, "libee.so")
 
 EE_F32, EE_BF16 = 0, 1
 EE_CAL_EXIT_RATE, EE_CAL_MEDIAN = 0, 1
+EE_CONF_MAXPROB, EE_CONF_MARGIN, EE_CONF_NEGENTROPY = 0, 1, 2
 _ERRNAMES = {-1: "EE_EINVAL", -2: "EE_ESTATE", -3: "EE_ENOMEM", -4: "EE_EHIP",
              -5: "EE_ECAPACITY", -6: "EE_EDEVICE"}
 
@@ -72,6 +73,7 @@ def _load():
         "ee_calibrate_threshold": (C.c_int, [V, _IP, _IP, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                              C.c_float, _FP]),
         "ee_set_readout_bias": (C.c_int, [V, C.c_int32, _FP, C.c_int32]),
+        "ee_set_confidence_measure": (C.c_int, [V, C.c_int32]),
         "ee_head_eval": (C.c_int, [V, C.c_int32, _FP, _IP, _FP, _FP]),
         "ee_read_kv": (C.c_int, [V, C.c_int32, C.c_int32, _FP, _FP]),
         "ee_set_persistent": (C.c_int, [V, C.c_int32]),
@@ -215,6 +217,9 @@ class Engine:
         b = np.ascontiguousarray(b, dtype=np.float32)
         self._b_keep = b  # the copy is asynchronous: keep the host buffer alive
         self._check(lib.ee_set_readout_bias(self._ctx, exit_layer, _ptr(b, C.c_float), 0))
+
+    def ee_set_confidence_measure(self, measure: int):
+        self._check(lib.ee_set_confidence_measure(self._ctx, measure))
 
     def ee_head_eval(self, readout_layer: int, x, want_logits: bool = True):
         x = np.ascontiguousarray(x, dtype=np.float32)

@@ -71,6 +71,7 @@ struct ee_ctx {
   int head_wgs = 0;
   int nwg_persistent = 0;
   int max_wgs_per_cu = 0;
+  int conf_measure = EE_CONF_MAXPROB;
   size_t lds = 0;
   hipEvent_t ev0 = nullptr, ev1 = nullptr;
   float last_ms = 0.f;
@@ -174,6 +175,7 @@ DevParams make_params(const ee_ctx* c, float tau, int exit_layer) {
   p.eps = g.rms_eps;
   p.attn_scale = static_cast<float>(1.0 / sqrt(static_cast<double>(p.D)));
   p.tau = tau;
+  p.conf_measure = c->conf_measure;
   p.exit_layer = exit_layer;
   p.page_size = g.page_size;
   int sh = 0;
@@ -605,7 +607,7 @@ int ee_create(const ee_config* cfg, void* hip_stream, ee_ctx** out) {
   c->persistent = c->nwg_persistent > 0;
   c->head_wgs = 2 * c->n_cu;
   c->max_parts = std::max(c->head_wgs, c->nwg_persistent);
-  if ((r = dalloc(c, &c->d_head_part, static_cast<size_t>(c->max_parts) * 4 * 4))) return bail(r);
+  if ((r = dalloc(c, &c->d_head_part, static_cast<size_t>(c->max_parts) * ee::kStatFloats * 4))) return bail(r);
   *out = c;
   return EE_OK;
 }
@@ -742,6 +744,15 @@ int ee_set_readout_bias(ee_ctx* c, int32_t exit_layer, const float* b, int32_t o
   if (it == c->readout.end() || !b) return fail(c, EE_EINVAL, "no readout at that layer");
   HIPCHK(c, hipMemcpyAsync(it->second.second, b, sizeof(float) * c->cfg.hidden,
                            on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice, c->stream));
+  return EE_OK;
+}
+
+int ee_set_confidence_measure(ee_ctx* c, int32_t measure) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  if (measure != EE_CONF_MAXPROB && measure != EE_CONF_MARGIN && measure != EE_CONF_NEGENTROPY)
+    return fail(c, EE_EINVAL, "unknown confidence measure");
+  c->conf_measure = measure;
   return EE_OK;
 }
 

@@ -15,6 +15,7 @@ constexpr int kMaxGroup = 8;           // max query heads per KV head
 constexpr int kMaxHeadDim = 256;
 constexpr int kBarGroups = 8;          // first level of the grid barrier (one per XCD)
 constexpr int kParamSlots = 16;        // persistent-kernel parameter blocks per device
+constexpr int kStatFloats = 6;         // a head partial (max, sum, second max, argmax, entropy term, pad)
 
 // Per-layer device pointers, repacked layouts:
 //   wqkv [(A + 2K) * D][H]: q rows, then k rows, then v rows. Within every q
@@ -72,6 +73,7 @@ struct DevParams {
   float eps;
   float attn_scale;             // 1/sqrt(D)
   float tau;
+  int conf_measure;             // gate confidence: 0 max-prob, 1 top-2 margin, 2 negative entropy
   int exit_layer;               // 0 = ungated
   int page_size, page_shift;
   // weights
@@ -101,7 +103,7 @@ struct DevParams {
   int64_t tw_words;
   uint64_t* attn_part;          // tagged attention partials [K][(G+1)/2][max_splits][2D + 4]
   int max_splits;
-  float* head_part;             // [max_parts][4]
+  float* head_part;             // [max_parts][kStatFloats]
   int max_parts;
   Counters* counters;
   StepCtl* ctl;

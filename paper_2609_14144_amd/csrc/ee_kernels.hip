@@ -642,7 +642,7 @@ __host__ __device__ inline int lds_vec_floats(const DevParams& p) {
   int v = p.H;
   if (p.F > v) v = p.F;
   if (p.A * p.D > v) v = p.A * p.D;
-  if (kWG * 4 > v) v = kWG * 4;
+  if (kWG * kStatFloats > v) v = kWG * kStatFloats;
   const int am = attn_lds_floats(p.D);
   if (am > v) v = am;
   return (v + 63) & ~63;
@@ -1180,18 +1180,23 @@ struct Stat {
   float s;    // sum of exp(logit - m)
   float m2;   // second largest logit (equal to m on ties)
   int idx;    // argmax, lowest index among ties
+  float t;    // sum of exp(logit - m) * (logit - m), for the entropy
 };
 
-__device__ inline Stat stat_empty() { return Stat{-INFINITY, 0.f, -INFINITY, 0x7fffffff}; }
+__device__ inline Stat stat_empty() { return Stat{-INFINITY, 0.f, -INFINITY, 0x7fffffff, 0.f}; }
 
 __device__ inline void stat_push(Stat& st, float v, int r) {
   if (v > st.m) {
-    st.s = st.s * expf(st.m - v) + 1.f;
+    const float sc = expf(st.m - v);
+    st.t = st.s > 0.f ? sc * (st.t + (st.m - v) * st.s) : 0.f;
+    st.s = st.s * sc + 1.f;
     st.m2 = st.m;
     st.m = v;
     st.idx = r;
   } else {
-    st.s += expf(v - st.m);
+    const float e = expf(v - st.m);
+    st.s += e;
+    st.t = fmaf(e, v - st.m, st.t);
     st.m2 = fmaxf(st.m2, v);
   }
 }
@@ -1202,9 +1207,30 @@ __device__ inline Stat stat_merge(Stat a, Stat b) {
   const bool bw = b.m > a.m || (b.m == a.m && b.idx < a.idx);
   Stat w = bw ? b : a;
   const Stat o = bw ? a : b;
-  w.s = w.s + o.s * expf(o.m - w.m);
+  const float sc = expf(o.m - w.m);
+  w.t = w.t + sc * (o.t + (o.m - w.m) * o.s);
+  w.s = w.s + o.s * sc;
   w.m2 = fmaxf(w.m2, o.m);
   return w;
+}
+
+__device__ inline void stat_put(float* d, const Stat& st) {
+  d[0] = st.m;
+  d[1] = st.s;
+  d[2] = st.m2;
+  d[3] = __int_as_float(st.idx);
+  d[4] = st.t;
+}
+__device__ inline Stat stat_get(const float* d) { return Stat{d[0], d[1], d[2], __float_as_int(d[3]), d[4]}; }
+
+// The confidence the gate compares with tau (Section 10 names three softmax
+// measures): 0 the best token's probability 1/s; 1 its margin over the
+// second best, (1 - exp(m2 - m)) / s; 2 the negative entropy
+// sum p log p = t/s - log s.
+__device__ inline float stat_confidence(const Stat& st, int measure) {
+  if (measure == 1) return (1.f - expf(st.m2 - st.m)) / st.s;
+  if (measure == 2) return st.t / st.s - logf(st.s);
+  return 1.f / st.s;
 }
 
 __device__ __forceinline__ int head_row(const DevParams& p, int wg, int nwg, int wave) {
@@ -1245,22 +1271,17 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
                                 for (int r = 0; r < nr; ++r) dbg[r0 + r] = acc[r];
                             }, 2);
   __shared__ int last_flag;
-  float* stl = xs;  // the normalised vector is no longer needed: kWG * 4 floats
+  float* stl = xs;  // the normalised vector is no longer needed: kWG * kStatFloats floats
   __syncthreads();
-  if (lane == 0) {
-    stl[wave * 4 + 0] = st.m;
-    stl[wave * 4 + 1] = st.s;
-    stl[wave * 4 + 2] = st.m2;
-    stl[wave * 4 + 3] = __int_as_float(st.idx);
-  }
+  if (lane == 0) stat_put(stl + wave * kStatFloats, st);
   __syncthreads();
   if (threadIdx.x == 0) {
     Stat tt = stat_empty();
-    for (int w = 0; w < kWaves; ++w)
-      tt = stat_merge(tt, Stat{stl[w * 4], stl[w * 4 + 1], stl[w * 4 + 2], __float_as_int(stl[w * 4 + 3])});
-    float* part = p.head_part + static_cast<int64_t>(wg) * 4;
+    for (int w = 0; w < kWaves; ++w) tt = stat_merge(tt, stat_get(stl + w * kStatFloats));
+    float* part = p.head_part + static_cast<int64_t>(wg) * kStatFloats;
     st_coh2(part, tt.m, tt.s);
     st_coh2(part + 2, tt.m2, __int_as_float(tt.idx));
+    st_coh2(part + 4, tt.t, 0.f);
     wait_stores();
     const uint32_t old = __hip_atomic_fetch_add(&p.counters->head[0], 1u, __ATOMIC_RELAXED,
                                                 __HIP_MEMORY_SCOPE_AGENT);
@@ -1271,13 +1292,14 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
   // the partials of up to 4 * kWG workgroups are loaded before any is merged
   Stat tt = stat_empty();
   for (int i0 = 0; i0 < nwg; i0 += 4 * kWG) {
-    uint64_t a[4], b[4];
+    uint64_t a[4], b[4], c[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int i = i0 + k * kWG + static_cast<int>(threadIdx.x);
-      const float* part = p.head_part + static_cast<int64_t>(min(i, nwg - 1)) * 4;
+      const float* part = p.head_part + static_cast<int64_t>(min(i, nwg - 1)) * kStatFloats;
       a[k] = ld_coh_u64(part);
       b[k] = ld_coh_u64(part + 2);
+      c[k] = ld_coh_u64(part + 4);
     }
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -1285,31 +1307,23 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
         tt = stat_merge(tt, Stat{__uint_as_float(static_cast<uint32_t>(a[k])),
                                  __uint_as_float(static_cast<uint32_t>(a[k] >> 32)),
                                  __uint_as_float(static_cast<uint32_t>(b[k])),
-                                 static_cast<int>(static_cast<uint32_t>(b[k] >> 32))});
+                                 static_cast<int>(static_cast<uint32_t>(b[k] >> 32)),
+                                 __uint_as_float(static_cast<uint32_t>(c[k]))});
     }
   }
-  stl[threadIdx.x * 4 + 0] = tt.m;
-  stl[threadIdx.x * 4 + 1] = tt.s;
-  stl[threadIdx.x * 4 + 2] = tt.m2;
-  stl[threadIdx.x * 4 + 3] = __int_as_float(tt.idx);
+  stat_put(stl + threadIdx.x * kStatFloats, tt);
   __syncthreads();
   for (int stride = kWG / 2; stride > 0; stride >>= 1) {
-    if (static_cast<int>(threadIdx.x) < stride) {
-      const float* a = stl + threadIdx.x * 4;
-      const float* b = stl + (threadIdx.x + stride) * 4;
-      const Stat r = stat_merge(Stat{a[0], a[1], a[2], __float_as_int(a[3])},
-                                Stat{b[0], b[1], b[2], __float_as_int(b[3])});
-      float* d = stl + threadIdx.x * 4;
-      d[0] = r.m;
-      d[1] = r.s;
-      d[2] = r.m2;
-      d[3] = __int_as_float(r.idx);
-    }
+    if (static_cast<int>(threadIdx.x) < stride)
+      stat_put(stl + threadIdx.x * kStatFloats,
+               stat_merge(stat_get(stl + threadIdx.x * kStatFloats),
+                          stat_get(stl + (threadIdx.x + stride) * kStatFloats)));
     __syncthreads();
   }
   if (threadIdx.x == 0) {
-    const int idx = __float_as_int(stl[3]);
-    const float conf = 1.f / stl[1];
+    const Stat fin = stat_get(stl);
+    const int idx = fin.idx;
+    const float conf = stat_confidence(fin, p.conf_measure);
     StepCtl* c = p.ctl;
     if (!sy.poll)
       __hip_atomic_store(&p.counters->head[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

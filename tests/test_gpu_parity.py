@@ -102,6 +102,72 @@ def test_tiny_decode_n_imposed_and_gated(persistent):
         assert e.ee_position() == TINY_P + TINY_N
 
 
+def measure_tol(measure, r):
+    """Allowed |device - oracle| for a step's confidence: the head's logits
+    carry fp32 errors of about 1e-4 relative (the max-prob bound below);
+    the margin inherits them through both probabilities, the negative
+    entropy through every log-probability (one per unit of entropy)."""
+    c = r.measures["maxprob"]
+    if measure == "maxprob":
+        return 1e-4 + 1e-3 * c
+    if measure == "margin":
+        return 1e-4 + 2e-3 * c
+    return 1e-3 * (1.0 + abs(r.conf))
+
+
+@pytest.mark.parametrize("persistent", [True, False], ids=["persistent", "per_op"])
+@pytest.mark.parametrize("measure", ["maxprob", "margin", "negentropy"])
+def test_tiny_confidence_measures(measure, persistent):
+    """The gate under each softmax confidence measure of Section 10, teacher
+    forced in one call: per-step confidence against the oracle's measure of
+    the readout distribution, decisions away from tau, and median
+    calibration on the device against the oracle's."""
+    from paper_2609_14144_amd import EE_CAL_MEDIAN
+    code = {"maxprob": 0, "margin": 1, "negentropy": 2}[measure]
+    name = "tiny_bf16"
+    cfg = synth.get_config(name)
+    prompt = synth.prompts(cfg, 1, TINY_P)
+    toks = synth.prompts(cfg, 6, TINY_N)
+    o = oracle_for(name, 128)
+    o.prefill(prompt)
+    ref = o.generate(None, math.inf, 2, TINY_N, force_tokens=toks, measure=measure)
+    tau = oracle.tau_median([r.conf for r in ref])
+    o = oracle_for(name, 128)
+    o.prefill(prompt)
+    rs = o.generate(None, tau, 2, TINY_N, force_tokens=toks, measure=measure)
+    e = engine(name, 128, persistent)
+    e.ee_set_confidence_measure(code)
+    e.ee_prefill(prompt)
+    tok, ex, conf, would = e.ee_decode_n_ex(tau, 2, TINY_N, force_tokens=toks)
+    decided = 0
+    for i, r in enumerate(rs):
+        assert abs(conf[i] - r.conf) <= measure_tol(measure, r), (i, conf[i], r.conf)
+        if abs(r.conf - tau) > MARGIN:
+            assert would[i] == r.would_exit and ex[i] == r.exited, i
+            decided += 1
+        gap = r.gap_readout if r.exited else r.gap_full
+        if gap > MARGIN and ex[i] == r.exited:
+            assert tok[i] == r.token, i
+    assert decided >= TINY_N // 2 and 0 < sum(r.exited for r in rs) < TINY_N
+    prompts = [synth.prompts(cfg, s, TINY_P) for s in range(100, 104)]
+    confs = []
+    for p in prompts:
+        o = oracle_for(name, 64)
+        confs += [r.conf for r in o.generate(o.prefill(p), math.inf, 2, TINY_N, measure=measure)]
+    e2 = engine(name, 64, persistent)
+    e2.ee_set_confidence_measure(code)
+    t_gpu = e2.ee_calibrate_threshold(prompts, TINY_N, 2, EE_CAL_MEDIAN, 0.0)
+    t_ref = oracle.tau_median(confs)
+    assert abs(t_gpu - t_ref) <= 2 * measure_tol(measure, rs[0]) + 1e-4
+
+
+def test_confidence_measure_rejects_unknown():
+    from paper_2609_14144_amd import EEError
+    e = engine("tiny_bf16", 32)
+    with pytest.raises(EEError):
+        e.ee_set_confidence_measure(3)
+
+
 def test_tiny_free_running_matches_until_first_margin():
     name = "tiny_bf16"
     cfg = synth.get_config(name)
@@ -417,3 +483,13 @@ def test_head_kernel_planted_ties_full_vocab():
             assert rg == 0.0 and tok == rj  # the planted tie: lowest id wins
         elif rg > MARGIN:
             assert tok == rj
+        # the other two measures from the same scan (Section 10)
+        m = oracle.confidence_measures(ref)
+        for code, key in ((1, "margin"), (2, "negentropy")):
+            e.ee_set_confidence_measure(code)
+            _, c2, _ = e.ee_head_eval(layer, x, want_logits=False)
+            tol = 1e-5 + 2e-4 * rc if key == "margin" else 1e-4 * (1.0 + abs(m[key]))
+            assert abs(c2 - m[key]) <= tol, (layer, key, c2, m[key])
+            if key == "margin" and layer == 0:
+                assert c2 == 0.0  # the planted tie
+        e.ee_set_confidence_measure(0)
