@@ -25,7 +25,7 @@ Parity status: every function is pinned by tests under tests/ (test_oracle_*).
 """
 from .numerics import round_to_storage, rmsnorm, rope, silu, head_stats, confidence_measures, MEASURES
 from .decoder import OracleDecoder, StepResult
-from .calibrate import tau_for_exit_rate, tau_median, nucleus_acceptable, tau_nucleus
+from .calibrate import tau_for_exit_rate, tau_median, nucleus_acceptable, nucleus_mass_ahead, tau_nucleus
 from . import costmodel
 
 __all__ = ["OracleDecoder", "StepResult", "round_to_storage", "rmsnorm", "rope", "silu",

@@ -46,13 +46,18 @@ def tau_median(confs) -> float:
     return float(np.float32(np.median(np.asarray(confs, dtype=np.float32).astype(np.float64))))
 
 
-def nucleus_acceptable(logits_full: np.ndarray, token: int, top_p: float = 0.9) -> bool:
+def nucleus_mass_ahead(logits_full: np.ndarray, token: int) -> float:
+    """Full-model probability mass strictly ahead of token in the order
+    (probability descending, id ascending)."""
     z = logits_full - logits_full.max()
     p = np.exp(z)
     p /= p.sum()
     pj = p[token]
-    ahead = p[(p > pj) | ((p == pj) & (np.arange(p.size) < token))].sum()
-    return bool(ahead < top_p)
+    return float(p[(p > pj) | ((p == pj) & (np.arange(p.size) < token))].sum())
+
+
+def nucleus_acceptable(logits_full: np.ndarray, token: int, top_p: float = 0.9) -> bool:
+    return nucleus_mass_ahead(logits_full, token) < top_p
 
 
 def tau_nucleus(confs, acceptable, required: float = 0.9) -> float:

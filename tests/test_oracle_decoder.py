@@ -256,6 +256,8 @@ def test_nucleus_acceptance_brute_force():
                 break
         for j in range(V):
             assert oracle.nucleus_acceptable(lg, j) == (j in nucleus), (V, j)
+            ahead = sum(p[t] for t in order[:order.index(j)])
+            assert oracle.nucleus_mass_ahead(lg, j) == pytest.approx(ahead, abs=1e-12)
 
 
 def test_tau_nucleus_grid():
