@@ -56,7 +56,10 @@ enum { EE_F32 = 0, EE_BF16 = 1 }; /* storage type of matrices and KV cache */
 
 enum {
   EE_CAL_EXIT_RATE = 0, /* tau so that a replay exits round(target*n) of n tokens */
-  EE_CAL_MEDIAN = 1     /* tau = median readout confidence (target ignored) */
+  EE_CAL_MEDIAN = 1,    /* tau = median readout confidence (target ignored) */
+  EE_CAL_NUCLEUS = 2    /* the paper's rule: lowest grid tau whose early answers are
+                           acceptable (inside the full model's 0.9 nucleus) at least
+                           a fraction target of the time */
 };
 
 /* Confidence measures the gate can compare with tau (Section 10 compares
@@ -112,6 +115,9 @@ typedef struct ee_debug {
   int32_t full_token;     /* full-head argmax, -1 when the upper layers were skipped */
   float conf;             /* readout max-probability (full head's when ungated) */
   float conf_full;        /* full head max-probability, NaN when skipped */
+  float nucleus_mass;     /* full-head probability ahead of readout_token (order: probability
+                             desc, id asc); readout_token is inside the 0.9 nucleus iff this
+                             is < 0.9. NaN when skipped or ungated */
 } ee_debug;
 
 typedef struct ee_ctx ee_ctx;
@@ -174,6 +180,12 @@ int ee_decode_step_ex(ee_ctx* ctx, float tau, int32_t exit_layer, int32_t input_
  * computed), recording the readout confidences. EE_CAL_EXIT_RATE: with the n
  * recorded values sorted ascending c_1..c_n and k = floor(target*n + 1/2),
  * tau = c_(n-k) (+inf for k = 0, -inf for k = n). EE_CAL_MEDIAN: the median.
+ * EE_CAL_NUCLEUS (Section 4 step four, Section 2 "Nucleus"): the final head
+ * also measures, per step, the full model's probability mass ahead of the
+ * readout's token; the token is acceptable iff that mass is below 0.9. tau is
+ * the smallest of 0.00, 0.01, ..., 0.99 for which the steps with confidence
+ * above tau are non-empty and acceptable with frequency >= target (the paper
+ * uses 0.9); +inf when none qualifies.
  * prompts holds the prompts back to back (host), prompt_lens their lengths.
  * Leaves the context reset. Errors: EE_EINVAL, EE_ESTATE, EE_ECAPACITY,
  * EE_EHIP, EE_EDEVICE. */

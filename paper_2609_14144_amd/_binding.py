@@ -13,7 +13,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 lib_path = os.path.join(_HERE, "libee.so")
 
 EE_F32, EE_BF16 = 0, 1
-EE_CAL_EXIT_RATE, EE_CAL_MEDIAN = 0, 1
+EE_CAL_EXIT_RATE, EE_CAL_MEDIAN, EE_CAL_NUCLEUS = 0, 1, 2
 EE_CONF_MAXPROB, EE_CONF_MARGIN, EE_CONF_NEGENTROPY = 0, 1, 2
 _ERRNAMES = {-1: "EE_EINVAL", -2: "EE_ESTATE", -3: "EE_ENOMEM", -4: "EE_EHIP",
              -5: "EE_ECAPACITY", -6: "EE_EDEVICE"}
@@ -45,7 +45,7 @@ class ee_debug(C.Structure):
     _fields_ = [("h_exit", _FP), ("h_final", _FP), ("logits_readout", _FP), ("logits_full", _FP),
                 ("token", C.c_int32), ("exited", C.c_int32), ("would_exit", C.c_int32),
                 ("readout_token", C.c_int32), ("full_token", C.c_int32), ("conf", C.c_float),
-                ("conf_full", C.c_float)]
+                ("conf_full", C.c_float), ("nucleus_mass", C.c_float)]
 
 
 def _load():
@@ -196,7 +196,7 @@ class Engine:
         self._check(lib.ee_decode_step_ex(self._ctx, tau, exit_layer, input_token, force_exit,
                                           C.byref(d)))
         out = {k: getattr(d, k) for k in ("token", "exited", "would_exit", "readout_token",
-                                          "full_token", "conf", "conf_full")}
+                                          "full_token", "conf", "conf_full", "nucleus_mass")}
         out["exited"] = bool(out["exited"])
         out["would_exit"] = bool(out["would_exit"])
         if debug:

@@ -60,6 +60,8 @@ struct ee_ctx {
   int ring_cap = 0;
   int32_t *d_ring_tok = nullptr, *d_ring_exit = nullptr, *d_ring_would = nullptr;
   float* d_ring_conf = nullptr;
+  float* d_ring_mass = nullptr;
+  bool nucleus = false;   // steps also measure the readout token's nucleus rank (calibration, debug)
   int force_cap = 0;
   int32_t *d_force_tok = nullptr, *d_force_exit = nullptr;
   float *d_dbg_r = nullptr, *d_dbg_f = nullptr, *d_x = nullptr;
@@ -83,6 +85,10 @@ struct ee_ctx {
 };
 
 namespace {
+
+// Section 2's nucleus: the smallest set of most probable tokens holding 0.9
+// of the full model's probability.
+constexpr float kNucleusTopP = 0.9f;
 
 thread_local std::string g_create_err;  // last ee_create failure (no context exists)
 std::atomic<uint32_t> g_slots{0};       // parameter slots in use (one bit each)
@@ -231,14 +237,16 @@ void reset_pages(ee_ctx* c) {
 int ensure_ring(ee_ctx* c, int n) {
   if (n <= c->ring_cap) return EE_OK;
   dfree(c->d_ring_tok); dfree(c->d_ring_exit); dfree(c->d_ring_would); dfree(c->d_ring_conf);
+  dfree(c->d_ring_mass);
   c->d_ring_tok = c->d_ring_exit = c->d_ring_would = nullptr;
-  c->d_ring_conf = nullptr;
+  c->d_ring_conf = c->d_ring_mass = nullptr;
   c->ring_cap = 0;
   int r;
   if ((r = dalloc(c, &c->d_ring_tok, sizeof(int32_t) * n))) return r;
   if ((r = dalloc(c, &c->d_ring_exit, sizeof(int32_t) * n))) return r;
   if ((r = dalloc(c, &c->d_ring_would, sizeof(int32_t) * n))) return r;
   if ((r = dalloc(c, &c->d_ring_conf, sizeof(float) * n))) return r;
+  if ((r = dalloc(c, &c->d_ring_mass, sizeof(float) * n))) return r;
   c->ring_cap = n;
   return EE_OK;
 }
@@ -279,6 +287,8 @@ int run_steps(ee_ctx* c, float tau, int exit_layer, int n, const int32_t* d_forc
   DevParams p = make_params(c, tau, prefill ? 0 : exit_layer);
   p.ring_tok = c->d_ring_tok; p.ring_exit = c->d_ring_exit;
   p.ring_would = c->d_ring_would; p.ring_conf = c->d_ring_conf;
+  p.ring_mass = c->d_ring_mass;
+  p.nucleus = c->nucleus && !prefill;
   p.force_tok = d_force_tok;
   p.force_exit = d_force_exit;
   if (debug) {
@@ -670,8 +680,10 @@ int ee_decode_step_ex(ee_ctx* c, float tau, int32_t exit_layer, int32_t input_to
   }
   const int32_t ft[1] = {input_token};
   const int32_t fe[1] = {force_exit};
+  c->nucleus = dbg != nullptr;
   r = decode_common(c, tau, exit_layer, 1, input_token >= 0 ? ft : nullptr,
                     force_exit >= 0 ? fe : nullptr, want_logits);
+  c->nucleus = false;
   if (r) return r;
   if (!dbg) return EE_OK;
   ee::StepCtl ctl;
@@ -687,6 +699,9 @@ int ee_decode_step_ex(ee_ctx* c, float tau, int32_t exit_layer, int32_t input_to
   dbg->readout_token = exit_layer > 0 ? ctl.readout_token : -1;
   dbg->full_token = ex ? -1 : ctl.full_token;
   dbg->conf_full = ex ? NAN : ctl.conf_full;
+  dbg->nucleus_mass = NAN;
+  if (!ex && exit_layer > 0)
+    HIPCHK(c, hipMemcpy(&dbg->nucleus_mass, c->d_ring_mass, sizeof(float), hipMemcpyDeviceToHost));
   if (dbg->h_exit && exit_layer > 0 && (r = copy_untag(c, dbg->h_exit, c->d_hexit, H))) return r;
   if (dbg->h_final && !ex && (r = copy_untag(c, dbg->h_final, c->d_h, H))) return r;
   if (dbg->logits_readout && exit_layer > 0)
@@ -704,24 +719,51 @@ int ee_calibrate_threshold(ee_ctx* c, const int32_t* prompts, const int32_t* pro
   if (!prompts || !prompt_lens || n_prompts <= 0 || n_gen <= 0 || !out_tau)
     return fail(c, EE_EINVAL, "calibration needs prompts, n_gen > 0 and an output");
   if (exit_layer < 1) return fail(c, EE_EINVAL, "calibration needs a gated exit layer");
-  if (mode != EE_CAL_EXIT_RATE && mode != EE_CAL_MEDIAN) return fail(c, EE_EINVAL, "unknown mode");
-  if (mode == EE_CAL_EXIT_RATE && !(target >= 0.f && target <= 1.f))
-    return fail(c, EE_EINVAL, "target exit rate must be in [0, 1]");
+  if (mode != EE_CAL_EXIT_RATE && mode != EE_CAL_MEDIAN && mode != EE_CAL_NUCLEUS)
+    return fail(c, EE_EINVAL, "unknown mode");
+  if (mode != EE_CAL_MEDIAN && !(target >= 0.f && target <= 1.f))
+    return fail(c, EE_EINVAL, "target must be in [0, 1]");
   int r;
   if ((r = check_gate_args(c, INFINITY, exit_layer))) return r;
-  std::vector<float> confs;
-  std::vector<float> buf(n_gen);
+  std::vector<float> confs, masses;
+  std::vector<float> buf(n_gen), mbuf(n_gen);
   size_t off = 0;
   for (int i = 0; i < n_prompts; ++i) {
     if (prompt_lens[i] <= 0) return fail(c, EE_EINVAL, "empty calibration prompt");
     if ((r = ee_reset(c))) return r;
     int32_t first = 0;
     if ((r = ee_prefill(c, prompts + off, prompt_lens[i], &first))) return r;
-    if ((r = ee_decode_n(c, INFINITY, exit_layer, n_gen, nullptr, nullptr, buf.data()))) return r;
+    c->nucleus = mode == EE_CAL_NUCLEUS;
+    r = ee_decode_n(c, INFINITY, exit_layer, n_gen, nullptr, nullptr, buf.data());
+    c->nucleus = false;
+    if (r) return r;
     confs.insert(confs.end(), buf.begin(), buf.end());
+    if (mode == EE_CAL_NUCLEUS) {
+      HIPCHK(c, hipMemcpy(mbuf.data(), c->d_ring_mass, sizeof(float) * n_gen, hipMemcpyDeviceToHost));
+      masses.insert(masses.end(), mbuf.begin(), mbuf.end());
+    }
     off += prompt_lens[i];
   }
   if ((r = ee_reset(c))) return r;
+  if (mode == EE_CAL_NUCLEUS) {
+    // the lowest grid threshold whose early answers are acceptable often enough
+    *out_tau = INFINITY;
+    for (int g = 0; g < 100; ++g) {
+      const float tau = static_cast<float>(g / 100.0);
+      size_t early = 0, ok = 0;
+      for (size_t i = 0; i < confs.size(); ++i) {
+        if (confs[i] > tau) {
+          ++early;
+          ok += masses[i] < kNucleusTopP;
+        }
+      }
+      if (early > 0 && static_cast<double>(ok) / static_cast<double>(early) >= static_cast<double>(target)) {
+        *out_tau = tau;
+        break;
+      }
+    }
+    return EE_OK;
+  }
   std::sort(confs.begin(), confs.end());
   const size_t n = confs.size();
   if (mode == EE_CAL_MEDIAN) {
@@ -926,7 +968,7 @@ void ee_destroy(ee_ctx* c) {
   dfree(c->d_cos); dfree(c->d_sin);
   dfree(c->d_tw);
   dfree(c->d_x); dfree(c->d_head_part); dfree(c->d_counters); dfree(c->d_ctl);
-  dfree(c->d_ring_tok); dfree(c->d_ring_exit); dfree(c->d_ring_would); dfree(c->d_ring_conf);
+  dfree(c->d_ring_tok); dfree(c->d_ring_exit); dfree(c->d_ring_would); dfree(c->d_ring_conf); dfree(c->d_ring_mass);
   dfree(c->d_force_tok); dfree(c->d_force_exit); dfree(c->d_dbg_r); dfree(c->d_dbg_f);
   dfree(c->d_timeline);
   if (c->ev0) (void)hipEventDestroy(c->ev0);

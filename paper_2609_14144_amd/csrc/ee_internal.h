@@ -15,7 +15,7 @@ constexpr int kMaxGroup = 8;           // max query heads per KV head
 constexpr int kMaxHeadDim = 256;
 constexpr int kBarGroups = 8;          // first level of the grid barrier (one per XCD)
 constexpr int kParamSlots = 16;        // persistent-kernel parameter blocks per device
-constexpr int kStatFloats = 6;         // a head partial (max, sum, second max, argmax, entropy term, pad)
+constexpr int kStatFloats = 6;         // a head partial (max, sum, second max, argmax, entropy term, mass ahead)
 
 // Per-layer device pointers, repacked layouts:
 //   wqkv [(A + 2K) * D][H]: q rows, then k rows, then v rows. Within every q
@@ -98,7 +98,7 @@ struct DevParams {
   uint64_t* o;                  // [A*D]
   uint64_t* a;                  // [F]
   uint64_t* kvnew;              // [2*K*D] this step's K row, then V row (storage-rounded)
-  uint64_t* dec;                // [4] exited, token, readout confidence, gate decision
+  uint64_t* dec;                // [5] exited, token, readout confidence, gate decision, readout token
   uint64_t* tw_all;             // all of the above, one block of tw_words words
   int64_t tw_words;
   uint64_t* attn_part;          // tagged attention partials [K][(G+1)/2][max_splits][2D + 4]
@@ -112,6 +112,8 @@ struct DevParams {
   int32_t* ring_exit;
   int32_t* ring_would;
   float* ring_conf;
+  float* ring_mass;             // full-head mass ahead of the readout token (when nucleus)
+  int nucleus;                  // the final head also measures the readout token's nucleus rank
   const int32_t* force_tok;     // may be null
   const int32_t* force_exit;    // may be null
   // debug outputs (device, may be null; only meaningful for single steps)

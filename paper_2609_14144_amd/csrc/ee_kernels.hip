@@ -1181,14 +1181,18 @@ struct Stat {
   float m2;   // second largest logit (equal to m on ties)
   int idx;    // argmax, lowest index among ties
   float t;    // sum of exp(logit - m) * (logit - m), for the entropy
+  float a;    // sum of exp(logit - m) over the tokens ahead of a reference token
 };
 
-__device__ inline Stat stat_empty() { return Stat{-INFINITY, 0.f, -INFINITY, 0x7fffffff, 0.f}; }
+__device__ inline Stat stat_empty() { return Stat{-INFINITY, 0.f, -INFINITY, 0x7fffffff, 0.f, 0.f}; }
 
-__device__ inline void stat_push(Stat& st, float v, int r) {
+// ahead: the token sorts before the reference token (higher logit, or equal
+// logit and lower id)
+__device__ inline void stat_push(Stat& st, float v, int r, bool ahead) {
   if (v > st.m) {
     const float sc = expf(st.m - v);
     st.t = st.s > 0.f ? sc * (st.t + (st.m - v) * st.s) : 0.f;
+    st.a = st.a * sc + (ahead ? 1.f : 0.f);
     st.s = st.s * sc + 1.f;
     st.m2 = st.m;
     st.m = v;
@@ -1197,6 +1201,7 @@ __device__ inline void stat_push(Stat& st, float v, int r) {
     const float e = expf(v - st.m);
     st.s += e;
     st.t = fmaf(e, v - st.m, st.t);
+    if (ahead) st.a += e;
     st.m2 = fmaxf(st.m2, v);
   }
 }
@@ -1209,6 +1214,7 @@ __device__ inline Stat stat_merge(Stat a, Stat b) {
   const Stat o = bw ? a : b;
   const float sc = expf(o.m - w.m);
   w.t = w.t + sc * (o.t + (o.m - w.m) * o.s);
+  w.a = w.a + o.a * sc;
   w.s = w.s + o.s * sc;
   w.m2 = fmaxf(w.m2, o.m);
   return w;
@@ -1220,8 +1226,11 @@ __device__ inline void stat_put(float* d, const Stat& st) {
   d[2] = st.m2;
   d[3] = __int_as_float(st.idx);
   d[4] = st.t;
+  d[5] = st.a;
 }
-__device__ inline Stat stat_get(const float* d) { return Stat{d[0], d[1], d[2], __float_as_int(d[3]), d[4]}; }
+__device__ inline Stat stat_get(const float* d) {
+  return Stat{d[0], d[1], d[2], __float_as_int(d[3]), d[4], d[5]};
+}
 
 // The confidence the gate compares with tau (Section 10 names three softmax
 // measures): 0 the best token's probability 1/s; 1 its margin over the
@@ -1261,12 +1270,40 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
   rmsnorm_stage(p, readout ? p.z : p.h, p.g_final, p.H, sy, xs, red);
   float* dbg = readout ? p.dbg_logits_r : p.dbg_logits_f;
   const int wave = wave_id(), lane = threadIdx.x & 63;
+  // Nucleus membership of the readout's token under the full head (Section
+  // 2): the mass of the tokens ahead of it. Its logit is computed the way
+  // the scan computes row nj (same lanes, same order), so the token is never
+  // ahead of itself.
+  __shared__ int sh_nj;
+  __shared__ float sh_lj;
+  int nj = -1;
+  float lj = 0.f;
+  if (!readout && p.nucleus && p.exit_layer > 0) {
+    if (threadIdx.x == 0)
+      sh_nj = sy.poll ? __float_as_int(tw_val(tw_wait(p, p.dec + 4, sy.tres, true))) : ld_coh(&p.ctl->readout_token);
+    __syncthreads();
+    nj = sh_nj;
+    if (wave == 0) {
+      const int nch = p.H / Elem<WT>::N;
+      RowBlock<WT, 1, CPL> rj;
+      rj.load(static_cast<const WT*>(p.embed), p.H, nj, 1, 0, nch);
+      float acc[1], tot[1] = {0.f};
+      rj.dot(xs, 1, 0, nch, acc);
+      tot[0] += acc[0];
+      wave_sum_n<1>(tot);
+      if (lane == 0) sh_lj = tot[0];
+    }
+    __syncthreads();
+    lj = sh_lj;
+  }
   Stat st = stat_empty();
   stream_tiles<WT, R, CPL>(static_cast<const WT*>(p.embed), p.H, HeadTask<WT, CPL, R>::tiling(p, wg, nwg),
                            xs, t.a, t.b, [&](int r0, int nr, const float(&acc)[R]) {
 #pragma unroll
                               for (int r = 0; r < R; ++r)
-                                if (r < nr) stat_push(st, acc[r], r0 + r);
+                                if (r < nr)
+                                  stat_push(st, acc[r], r0 + r,
+                                            nj >= 0 && (acc[r] > lj || (acc[r] == lj && r0 + r < nj)));
                               if (dbg && lane == 0)
                                 for (int r = 0; r < nr; ++r) dbg[r0 + r] = acc[r];
                             }, 2);
@@ -1281,7 +1318,7 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
     float* part = p.head_part + static_cast<int64_t>(wg) * kStatFloats;
     st_coh2(part, tt.m, tt.s);
     st_coh2(part + 2, tt.m2, __int_as_float(tt.idx));
-    st_coh2(part + 4, tt.t, 0.f);
+    st_coh2(part + 4, tt.t, tt.a);
     wait_stores();
     const uint32_t old = __hip_atomic_fetch_add(&p.counters->head[0], 1u, __ATOMIC_RELAXED,
                                                 __HIP_MEMORY_SCOPE_AGENT);
@@ -1308,7 +1345,8 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
                                  __uint_as_float(static_cast<uint32_t>(a[k] >> 32)),
                                  __uint_as_float(static_cast<uint32_t>(b[k])),
                                  static_cast<int>(static_cast<uint32_t>(b[k] >> 32)),
-                                 __uint_as_float(static_cast<uint32_t>(c[k]))});
+                                 __uint_as_float(static_cast<uint32_t>(c[k])),
+                                 __uint_as_float(static_cast<uint32_t>(c[k] >> 32))});
     }
   }
   stat_put(stl + threadIdx.x * kStatFloats, tt);
@@ -1334,6 +1372,7 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
       // the gate record every workgroup reads: exited, token, confidence, decision
       tw_store(p.dec + 2, conf, sy.tout);
       tw_store(p.dec + 3, __int_as_float(would), sy.tout);
+      tw_store(p.dec + 4, __int_as_float(idx), sy.tout);
       if (ex) tw_store(p.dec + 1, __int_as_float(idx), sy.tout);
       tw_store(p.dec + 0, __int_as_float(ex), sy.tout);
       st_coh(&c->readout_token, idx);
@@ -1369,6 +1408,7 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
         p.ring_exit[step] = 0;
         p.ring_conf[step] = rconf;
         p.ring_would[step] = rwould;
+        if (nj >= 0 && p.ring_mass) p.ring_mass[step] = fin.a / fin.s;
       }
     }
   }

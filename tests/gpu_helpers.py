@@ -51,6 +51,20 @@ def check_vec(tag, got, ref, report):
     assert r <= TIGHT, (tag, r)
 
 
+def check_nucleus_mass(i, got, logits_full, token):
+    """Full-head mass ahead of the readout's token against the oracle. Tokens
+    whose logit is within rounding of the token's may sort on either side of
+    it: their probability is allowed on top of the fp32 tolerance."""
+    ref = oracle.nucleus_mass_ahead(logits_full, token)
+    lj = logits_full[token]
+    p = np.exp(logits_full - logits_full.max())
+    p /= p.sum()
+    close = np.abs(logits_full - lj) <= 1e-3 * max(1.0, abs(lj))
+    close[token] = False
+    assert abs(got - ref) <= 1e-4 + 2e-3 * ref + p[close].sum(), (i, got, ref)
+    return ref
+
+
 def compare_step(i, d, r, tau, report, check_vectors=True):
     """d: GPU debug dict from ee_decode_step_ex; r: oracle StepResult (same
     input token and imposed branch). Returns True if the step was outside
@@ -74,6 +88,8 @@ def compare_step(i, d, r, tau, report, check_vectors=True):
         else:
             comparable = False
         assert abs(d["conf_full"] - r.conf_full) <= 1e-4 + 1e-3 * r.conf_full
+        if r.readout_token >= 0 and r.gap_readout > MARGIN and r.logits_full is not None:
+            check_nucleus_mass(i, d["nucleus_mass"], r.logits_full, r.readout_token)
     elif r.gap_readout > MARGIN:
         assert d["token"] == r.token
     if check_vectors:

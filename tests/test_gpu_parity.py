@@ -8,7 +8,7 @@ import pytest
 import oracle
 import synth
 from tests.conftest import weights_for
-from tests.gpu_helpers import (MARGIN, compare_step, engine, lockstep, oracle_for, rel)
+from tests.gpu_helpers import (MARGIN, check_nucleus_mass, compare_step, engine, lockstep, oracle_for, rel)
 
 pytestmark = pytest.mark.gpu
 
@@ -159,6 +159,63 @@ def test_tiny_confidence_measures(measure, persistent):
     t_gpu = e2.ee_calibrate_threshold(prompts, TINY_N, 2, EE_CAL_MEDIAN, 0.0)
     t_ref = oracle.tau_median(confs)
     assert abs(t_gpu - t_ref) <= 2 * measure_tol(measure, rs[0]) + 1e-4
+
+
+@pytest.mark.parametrize("persistent", [True, False], ids=["persistent", "per_op"])
+def test_tiny_nucleus_mass(persistent):
+    """The full head's probability mass ahead of the readout's token (its
+    nucleus rank, Section 2), measured in the same vocabulary scan, against
+    the oracle on teacher-forced fallback steps."""
+    name = "tiny_bf16"
+    cfg = synth.get_config(name)
+    prompt = synth.prompts(cfg, 1, TINY_P)
+    toks = synth.prompts(cfg, 6, 12)
+    o = oracle_for(name, 64)
+    o.prefill(prompt)
+    e = engine(name, 64, persistent)
+    e.ee_prefill(prompt)
+    inside = 0
+    for i, t in enumerate(toks):
+        r = o.decode_step(int(t), math.inf, 2, keep_logits=True)
+        d = e.ee_decode_step_ex(math.inf, 2, int(t), -1, debug=False)
+        assert not d["exited"]
+        if r.gap_readout > MARGIN:
+            assert d["readout_token"] == r.readout_token
+            inside += check_nucleus_mass(i, d["nucleus_mass"], r.logits_full, r.readout_token) < 0.9
+    print("tiny nucleus: readout token inside the 0.9 nucleus on", inside, "of", len(toks), "steps")
+
+
+@pytest.mark.parametrize("persistent", [True, False], ids=["persistent", "per_op"])
+def test_tiny_nucleus_calibration(persistent):
+    """The paper's calibration rule (Section 4 step four): the lowest grid
+    threshold whose early answers lie inside the full model's 0.9 nucleus
+    often enough, on the device against the oracle's rule on its own
+    confidences and masses."""
+    from paper_2609_14144_amd import EE_CAL_NUCLEUS
+    name = "tiny_bf16"
+    cfg = synth.get_config(name)
+    prompts = [synth.prompts(cfg, s, TINY_P) for s in range(100, 104)]
+    confs, masses = [], []
+    for p in prompts:
+        o = oracle_for(name, 64)
+        for r in o.generate(o.prefill(p), math.inf, 2, TINY_N, keep_logits=True):
+            confs.append(r.conf)
+            masses.append(oracle.nucleus_mass_ahead(r.logits_full, r.readout_token))
+    confs, masses = np.array(confs), np.array(masses)
+    e = engine(name, 64, persistent)
+    for target in (0.3, 0.6, 0.9):
+        t_ref = oracle.tau_nucleus(confs, masses < 0.9, required=float(np.float32(target)))
+        t_gpu = e.ee_calibrate_threshold(prompts, TINY_N, 2, EE_CAL_NUCLEUS, target)
+        # the rule is discontinuous: compare only where no step sits within
+        # the comparison margin of 0.9 or of a grid threshold at or below t_ref
+        g = np.arange(100) / 100.0
+        below = g[g <= (t_ref if math.isfinite(t_ref) else 1.0)]
+        near = np.any(np.abs(masses - 0.9) <= MARGIN) or np.any(
+            np.abs(confs[:, None] - below[None, :]) <= MARGIN)
+        print("nucleus target", target, "tau gpu", t_gpu, "oracle", t_ref, "ambiguous", near)
+        if not near:
+            assert t_gpu == t_ref or (math.isinf(t_gpu) and math.isinf(t_ref))
+    assert e.ee_position() == 0
 
 
 def test_confidence_measure_rejects_unknown():
