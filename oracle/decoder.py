@@ -95,12 +95,14 @@ class OracleDecoder:
         shape = (cfg.n_layers, max_seq, cfg.n_kv_heads, cfg.head_dim)
         self.kcache = np.zeros(shape)
         self.vcache = np.zeros(shape)
+        self.hist = np.full(max_seq, -1, dtype=np.int64)  # input token of every position
         self.pos = 0
 
     # -- bookkeeping -------------------------------------------------------
     def reset(self):
         self.kcache[:] = 0.0
         self.vcache[:] = 0.0
+        self.hist[:] = -1
         self.pos = 0
 
     def _store(self, l, t, k, v):
@@ -173,6 +175,7 @@ class OracleDecoder:
         t = self.pos
         if t >= self.max_seq:
             raise ValueError("cache capacity exceeded")
+        self.hist[t] = token
         h = self.E[token].copy()
         for l in range(exit_layer):
             h = self.layer(l, h, t)
@@ -220,6 +223,7 @@ class OracleDecoder:
         if t0 + P > self.max_seq:
             raise ValueError("cache capacity exceeded")
         T = t0 + P
+        self.hist[t0:T] = tokens
         pos = np.arange(t0, T)
         group = c.n_q_heads // c.n_kv_heads
         H = self.E[tokens].copy()
@@ -246,6 +250,21 @@ class OracleDecoder:
         self.pos = T
         self.last_prefill_stats = head_stats(self.full_logits(H[-1]))  # (token, conf, gap)
         return self.last_prefill_stats[0]
+
+    def refresh(self, n: int) -> None:
+        """Full-depth pass over the n most recent positions with their own
+        input tokens: their cache entries at every layer are recomputed
+        exactly, replacing the entries the KV-absence fill projected for
+        exited tokens (Section 10: a periodic full-depth pass over the most
+        recent tokens recovers the drift of the reconstructed cache). The
+        position and the next input are unchanged."""
+        if not (1 <= n <= self.pos):
+            raise ValueError("refresh needs 1 <= n <= position")
+        end = self.pos
+        toks = self.hist[end - n:end].copy()
+        self.pos = end - n
+        self.prefill(toks)
+        assert self.pos == end
 
     def generate(self, first_token: int, tau: float, exit_layer: int, n: int,
                  force_tokens=None, force_exit=None, keep_logits=False, measure="maxprob"):

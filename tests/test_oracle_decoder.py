@@ -266,3 +266,33 @@ def test_tau_nucleus_grid():
     # early set at tau=0.2 is {0.35..0.95}: all acceptable; at tau=0.05..0.19 one of 6 fails (5/6 < .9)
     assert oracle.tau_nucleus(confs, ok) == pytest.approx(0.2)
     assert oracle.tau_nucleus(confs, np.zeros(7, bool)) == math.inf
+
+
+def test_refresh_restores_the_full_depth_cache(w):
+    """A full-depth pass over every decoded position (Section 10's periodic
+    refresh) replaces the projected entries of exited tokens with the cache
+    an ungated run over the same tokens writes; the next step then matches
+    the ungated model's."""
+    toks = seq(12, 5)
+    a = oracle.OracleDecoder(CFG, w, 64)
+    a.prefill(seq(P, 1))
+    ra = a.generate(None, 0.0, 2, 12, force_tokens=toks)        # every step exits
+    assert all(r.exited for r in ra)
+    b = oracle.OracleDecoder(CFG, w, 64)
+    b.prefill(seq(P, 1))
+    b.generate(None, 0.5, 0, 12, force_tokens=toks)              # ungated, full depth
+    up = slice(2, CFG.n_layers)
+    span = slice(P, P + 12)
+    assert rel(a.kcache[up, span], b.kcache[up, span]) > 1e-2    # projected entries differ
+    np.testing.assert_array_equal(a.hist[:P + 12], b.hist[:P + 12])
+    a.refresh(12)
+    assert a.pos == P + 12
+    assert rel(a.kcache[:, :P + 12], b.kcache[:, :P + 12]) < 1e-12
+    assert rel(a.vcache[:, :P + 12], b.vcache[:, :P + 12]) < 1e-12
+    na = a.decode_step(int(toks[0]), 0.5, 0)
+    nb = b.decode_step(int(toks[0]), 0.5, 0)
+    assert na.token == nb.token and rel(na.h_final, nb.h_final) < 1e-12
+    with pytest.raises(ValueError):
+        a.refresh(0)
+    with pytest.raises(ValueError):
+        a.refresh(a.pos + 1)
