@@ -210,6 +210,15 @@ def main():
         results["ungated"] = run_condition(e, cfg, math.inf, 0, prompt, args.warmup, args.steps)
         log(f"ungated: {results['ungated']}")
     head = results["r0.5"]
+    # periodic full-depth refresh (Section 10) of the 16 most recent positions,
+    # after the last timed run: one launch of 16 full-depth steps
+    rms = []
+    for _ in range(3):
+        e.ee_refresh(16)
+        rms.append(e.ee_last_decode_ms())
+    results["refresh16"] = {"positions": 16, "kernel_ms": sorted(rms)[1],
+                            "full_depth_steps_equivalent": 16}
+    log(f"refresh of 16 positions: {results['refresh16']}")
 
     kname = "k_decode_persistent" if args.program == "persistent" else "per_op"
     per_launch = head["algorithmic_bytes"]

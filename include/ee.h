@@ -193,6 +193,15 @@ int ee_calibrate_threshold(ee_ctx* ctx, const int32_t* prompts, const int32_t* p
                            int32_t n_prompts, int32_t n_gen, int32_t exit_layer,
                            int32_t mode, float target, float* out_tau);
 
+/* Periodic full-depth refresh (Section 10): recompute the cache entries of
+ * the n most recent positions at every layer from their own input tokens,
+ * replacing the entries projected for exited tokens by the KV-absence fill.
+ * Runs the prompt program (full depth, ungated) over those positions, one
+ * position after another: it costs n full-depth steps. The position and the
+ * next input token are unchanged. Errors: EE_EINVAL (n outside
+ * 1..position), EE_ESTATE, EE_EHIP, EE_EDEVICE. */
+int ee_refresh(ee_ctx* ctx, int32_t n);
+
 /* Select the confidence measure (EE_CONF_*) for the gate (exit iff the
  * measure exceeds tau), for the conf values decode calls report, for
  * calibration and for ee_head_eval. All three come from the same single pass

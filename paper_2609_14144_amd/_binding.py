@@ -74,6 +74,7 @@ def _load():
                                              C.c_float, _FP]),
         "ee_set_readout_bias": (C.c_int, [V, C.c_int32, _FP, C.c_int32]),
         "ee_set_confidence_measure": (C.c_int, [V, C.c_int32]),
+        "ee_refresh": (C.c_int, [V, C.c_int32]),
         "ee_head_eval": (C.c_int, [V, C.c_int32, _FP, _IP, _FP, _FP]),
         "ee_read_kv": (C.c_int, [V, C.c_int32, C.c_int32, _FP, _FP]),
         "ee_set_persistent": (C.c_int, [V, C.c_int32]),
@@ -217,6 +218,9 @@ class Engine:
         b = np.ascontiguousarray(b, dtype=np.float32)
         self._b_keep = b  # the copy is asynchronous: keep the host buffer alive
         self._check(lib.ee_set_readout_bias(self._ctx, exit_layer, _ptr(b, C.c_float), 0))
+
+    def ee_refresh(self, n: int):
+        self._check(lib.ee_refresh(self._ctx, n))
 
     def ee_set_confidence_measure(self, measure: int):
         self._check(lib.ee_set_confidence_measure(self._ctx, measure))

@@ -39,6 +39,7 @@ struct ee_ctx {
   int64_t layer_stride = 0;
   int n_pages = 0;
   int32_t* d_block_table = nullptr;
+  int32_t* d_hist = nullptr;         // input token of every position
   int32_t* h_block_table = nullptr;  // pinned
   int pages_mapped = 0;
   std::vector<int32_t> free_pages;
@@ -197,6 +198,7 @@ DevParams make_params(const ee_ctx* c, float tau, int exit_layer) {
   }
   p.kpool = c->kpool; p.vpool = c->vpool; p.layer_stride = c->layer_stride;
   p.block_table = c->d_block_table;
+  p.hist_tok = c->d_hist;
   p.rope_cos = c->d_cos; p.rope_sin = c->d_sin;
   p.h = c->d_h; p.h_exit = c->d_hexit; p.z = c->d_z; p.q = c->d_q; p.o = c->d_o; p.a = c->d_a;
   p.kvnew = c->d_kvnew; p.dec = c->d_dec; p.tw_all = c->d_tw; p.tw_words = c->tw_words;
@@ -594,6 +596,7 @@ int ee_create(const ee_config* cfg, void* hip_stream, ee_ctx** out) {
     }
     if ((he = hipMemset(c->d_tw, 0, total * 8)) != hipSuccess) return bail(hip_fail(c, he, "hipMemset"));
   }
+  if ((r = dalloc(c, &c->d_hist, sizeof(int32_t) * g.max_seq))) return bail(r);
   if ((r = dalloc(c, &c->d_counters, sizeof(ee::Counters)))) return bail(r);
   if ((r = dalloc(c, &c->d_ctl, sizeof(ee::StepCtl)))) return bail(r);
 
@@ -646,6 +649,31 @@ int ee_prefill(ee_ctx* c, const int32_t* tokens, int32_t n, int32_t* out_first_t
   int32_t tok = -1;
   HIPCHK(c, hipMemcpy(&tok, c->d_ring_tok + (n - 1), sizeof(tok), hipMemcpyDeviceToHost));
   if (out_first_token) *out_first_token = tok;
+  return EE_OK;
+}
+
+int ee_refresh(ee_ctx* c, int32_t n) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  if (!weights_ready(c)) return fail(c, EE_ESTATE, "weights not fully loaded");
+  if (n < 1 || n > c->pos) return fail(c, EE_EINVAL, "refresh needs 1 <= n <= position");
+  int r;
+  if ((r = ensure_force(c, n))) return r;
+  HIPCHK(c, hipMemcpyAsync(c->d_force_tok, c->d_hist + (c->pos - n), sizeof(int32_t) * n,
+                           hipMemcpyDeviceToDevice, c->stream));
+  int32_t next = 0;
+  HIPCHK(c, hipMemcpy(&next, &c->d_ctl->next_token, sizeof(next), hipMemcpyDeviceToHost));
+  const bool had = c->have_next;
+  c->pos -= n;
+  r = run_steps(c, INFINITY, 0, n, c->d_force_tok, nullptr, true, false);
+  if (r) {
+    c->pos += n;
+    c->have_next = false;
+    return r;
+  }
+  // the pass's own head output is not an emitted token: the next input stays
+  HIPCHK(c, hipMemcpy(&c->d_ctl->next_token, &next, sizeof(next), hipMemcpyHostToDevice));
+  c->have_next = had;
   return EE_OK;
 }
 
@@ -963,7 +991,7 @@ void ee_destroy(ee_ctx* c) {
     dfree(kv.second.first);
     dfree(kv.second.second);
   }
-  dfree(c->d_layers); dfree(c->kpool); dfree(c->vpool); dfree(c->d_block_table);
+  dfree(c->d_layers); dfree(c->kpool); dfree(c->vpool); dfree(c->d_block_table); dfree(c->d_hist);
   if (c->h_block_table) (void)hipHostFree(c->h_block_table);
   dfree(c->d_cos); dfree(c->d_sin);
   dfree(c->d_tw);

@@ -87,6 +87,7 @@ struct DevParams {
   void* vpool;
   int64_t layer_stride;         // elements per layer
   const int32_t* block_table;   // logical page -> physical page
+  int32_t* hist_tok;            // [max_seq] input token of every position (written by layer 0)
   const float* rope_cos;        // [max_seq][D/2]
   const float* rope_sin;
   // Activations passed between phases, as tagged words: low 32 bits the fp32

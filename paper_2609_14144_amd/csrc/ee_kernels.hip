@@ -576,6 +576,7 @@ __device__ void phase_qkv(const DevParams& p, int l, int pos, int step, int wg, 
     // layer 0 starts from the token's embedding row; workgroup 0 also
     // publishes it as the residual stream h
     const int tok = step_token(p, step, sy);
+    if (wg == 0 && threadIdx.x == 0 && p.hist_tok) p.hist_tok[pos] = tok;  // read after the launch
     const WT* e = static_cast<const WT*>(p.embed) + static_cast<int64_t>(tok) * p.H;
     __syncthreads();
     float ss = 0.f;

@@ -56,7 +56,7 @@ def _bench_json(path):
 def _timed(dispatches, bench):
     """The decode dispatches of the timed launches: for each condition of the
     sweep, in order, the first decode dispatch after bench.py's marker."""
-    conds = list(bench["sweep"].items())
+    conds = [(k, c) for k, c in bench["sweep"].items() if "realised_exit_rate" in c]
     rows = sorted(dispatches, key=lambda d: int(d["Dispatch_Id"]))
     out = []
     marks = [i for i, d in enumerate(rows) if MARKER_KERNEL in d["Kernel_Name"]]

@@ -117,3 +117,28 @@ def lockstep(e, o, first_token, tau, exit_layer, n, force_tokens=None, force_exi
         outside += compare_step(i, d, r, tau, report)
         tok = r.token
     return report, outside
+
+
+def check_kv(e, o, cfg, layers, positions):
+    """Cache entries read back through the ABI against the oracle's cache."""
+    for l in layers:
+        for t in positions:
+            k, v = e.ee_read_kv(l, t)
+            for got, ref in ((k, o.kcache[l, t].reshape(-1)), (v, o.vcache[l, t].reshape(-1))):
+                err = np.abs(got - ref)
+                scale = np.max(np.abs(ref))
+                if cfg.wdtype == "f32":
+                    # fp32 accumulation over H terms: a few ulps of the vector's scale
+                    assert np.all(err <= 1e-5 * scale), (l, t, float(err.max()))
+                    continue
+                # Both sides store the cache in bf16. Where an fp32 value sat within
+                # accumulation noise of a rounding midpoint the two round apart by one
+                # step of the element, and that difference in an earlier layer or
+                # position perturbs later entries by about one bf16 step of the
+                # vector's scale. A wrong position, layer, rotation or a missing fill
+                # is off by the order of the values themselves.
+                tol = (np.abs(ref) + scale) * 2.0 ** -7 * 1.01
+                assert np.all(err <= tol), (l, t, float(err.max()))
+                rms = np.sqrt(np.mean(err ** 2) / np.mean(ref ** 2))
+                assert rms <= 2.0 ** -8, (l, t, float(rms))
+

@@ -8,7 +8,8 @@ import pytest
 import oracle
 import synth
 from tests.conftest import weights_for
-from tests.gpu_helpers import (MARGIN, check_nucleus_mass, compare_step, engine, lockstep, oracle_for, rel)
+from tests.gpu_helpers import (MARGIN, check_kv, check_nucleus_mass, compare_step, engine, lockstep,
+                               oracle_for, rel)
 
 pytestmark = pytest.mark.gpu
 
@@ -257,26 +258,39 @@ def test_kv_cache_contents_including_fill(name):
     e = engine(name, 64, page_size=16)
     e.ee_prefill(prompt)
     e.ee_decode_n_ex(0.5, 2, 8, force_tokens=toks, force_exit=fe)
-    for l in range(cfg.n_layers):
-        for t in range(TINY_P + 8):
-            k, v = e.ee_read_kv(l, t)
-            for got, ref in ((k, o.kcache[l, t].reshape(-1)), (v, o.vcache[l, t].reshape(-1))):
-                err = np.abs(got - ref)
-                scale = np.max(np.abs(ref))
-                if cfg.wdtype == "f32":
-                    # fp32 accumulation over H terms: a few ulps of the vector's scale
-                    assert np.all(err <= 1e-5 * scale), (l, t, float(err.max()))
-                    continue
-                # Both sides store the cache in bf16. Where an fp32 value sat within
-                # accumulation noise of a rounding midpoint the two round apart by one
-                # step of the element, and that difference in an earlier layer or
-                # position perturbs later entries by about one bf16 step of the
-                # vector's scale. A wrong position, layer, rotation or a missing fill
-                # is off by the order of the values themselves.
-                tol = (np.abs(ref) + scale) * 2.0 ** -7 * 1.01
-                assert np.all(err <= tol), (l, t, float(err.max()))
-                rms = np.sqrt(np.mean(err ** 2) / np.mean(ref ** 2))
-                assert rms <= 2.0 ** -8, (l, t, float(rms))
+    check_kv(e, o, cfg, range(cfg.n_layers), range(TINY_P + 8))
+
+
+@pytest.mark.parametrize("persistent", [True, False], ids=["persistent", "per_op"])
+def test_refresh_recomputes_the_cache(persistent):
+    """Periodic full-depth refresh (Section 10): after a run where every token
+    exits, a refresh of the decoded positions rewrites their cache entries at
+    every layer as the oracle's refresh does (which equals an ungated run);
+    position and next input are kept and the following steps match."""
+    from paper_2609_14144_amd import EEError
+    name = "tiny_bf16"
+    cfg = synth.get_config(name)
+    prompt = synth.prompts(cfg, 1, TINY_P)
+    toks = synth.prompts(cfg, 7, 12)
+    o = oracle_for(name, 64)
+    o.prefill(prompt)
+    rs = o.generate(None, 0.0, 2, 12, force_tokens=toks)
+    e = engine(name, 64, persistent, page_size=16)
+    e.ee_prefill(prompt)
+    tok, ex, conf, would = e.ee_decode_n_ex(0.0, 2, 12, force_tokens=toks)
+    assert ex.all()
+    o.refresh(12)
+    e.ee_refresh(12)
+    assert e.ee_position() == TINY_P + 12
+    check_kv(e, o, cfg, range(cfg.n_layers), range(TINY_P, TINY_P + 12))
+    # the next input is still the last emitted token
+    nxt = o.decode_step(rs[-1].token, 0.5, 2, keep_logits=True)
+    d = e.ee_decode_step_ex(0.5, 2, -1, int(nxt.exited))
+    compare_step(0, d, nxt, 0.5, [])
+    rep, _ = lockstep(e, o, None, 0.5, 2, 3, force_tokens=synth.prompts(cfg, 8, 3))
+    for n in (0, e.ee_position() + 1):
+        with pytest.raises(EEError):
+            e.ee_refresh(n)
 
 
 def test_error_paths():
