@@ -62,6 +62,12 @@ enum {
                            a fraction target of the time */
 };
 
+/* When the KV-absence fill of an exited token runs (Section 4 step five). */
+enum {
+  EE_FILL_EAGER = 0, /* in the exit step itself (the default) */
+  EE_FILL_LAZY = 1   /* deferred and batched: see ee_set_fill_policy */
+};
+
 /* Confidence measures the gate can compare with tau (Section 10 compares
  * these three softmax measures of the readout's distribution p). */
 enum {
@@ -201,6 +207,16 @@ int ee_calibrate_threshold(ee_ctx* ctx, const int32_t* prompts, const int32_t* p
  * next input token are unchanged. Errors: EE_EINVAL (n outside
  * 1..position), EE_ESTATE, EE_EHIP, EE_EDEVICE. */
 int ee_refresh(ee_ctx* ctx, int32_t n);
+
+/* EE_FILL_LAZY: in the persistent program an exit step only keeps its
+ * exit-layer state; the cache entries of consecutive exited tokens are
+ * written together (each skipped layer's W_k/W_v rows read once per batch)
+ * before the next step that runs the upper layers, when the batch is full
+ * (up to 8 tokens, fewer for wide models) and before the call returns, so
+ * the cache is complete whenever a call has returned. The entries are
+ * bit-identical to the eager fill's. The one-kernel-per-operation program
+ * always fills eagerly. Errors: EE_EINVAL (unknown policy). */
+int ee_set_fill_policy(ee_ctx* ctx, int32_t policy);
 
 /* Select the confidence measure (EE_CONF_*) for the gate (exit iff the
  * measure exceeds tau), for the conf values decode calls report, for

@@ -15,6 +15,7 @@ lib_path = os.path.join(_HERE, "libee.so")
 EE_F32, EE_BF16 = 0, 1
 EE_CAL_EXIT_RATE, EE_CAL_MEDIAN, EE_CAL_NUCLEUS = 0, 1, 2
 EE_CONF_MAXPROB, EE_CONF_MARGIN, EE_CONF_NEGENTROPY = 0, 1, 2
+EE_FILL_EAGER, EE_FILL_LAZY = 0, 1
 _ERRNAMES = {-1: "EE_EINVAL", -2: "EE_ESTATE", -3: "EE_ENOMEM", -4: "EE_EHIP",
              -5: "EE_ECAPACITY", -6: "EE_EDEVICE"}
 
@@ -75,6 +76,7 @@ def _load():
         "ee_set_readout_bias": (C.c_int, [V, C.c_int32, _FP, C.c_int32]),
         "ee_set_confidence_measure": (C.c_int, [V, C.c_int32]),
         "ee_refresh": (C.c_int, [V, C.c_int32]),
+        "ee_set_fill_policy": (C.c_int, [V, C.c_int32]),
         "ee_head_eval": (C.c_int, [V, C.c_int32, _FP, _IP, _FP, _FP]),
         "ee_read_kv": (C.c_int, [V, C.c_int32, C.c_int32, _FP, _FP]),
         "ee_set_persistent": (C.c_int, [V, C.c_int32]),
@@ -218,6 +220,9 @@ class Engine:
         b = np.ascontiguousarray(b, dtype=np.float32)
         self._b_keep = b  # the copy is asynchronous: keep the host buffer alive
         self._check(lib.ee_set_readout_bias(self._ctx, exit_layer, _ptr(b, C.c_float), 0))
+
+    def ee_set_fill_policy(self, policy: int):
+        self._check(lib.ee_set_fill_policy(self._ctx, policy))
 
     def ee_refresh(self, n: int):
         self._check(lib.ee_refresh(self._ctx, n))

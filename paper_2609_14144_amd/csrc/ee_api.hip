@@ -62,6 +62,8 @@ struct ee_ctx {
   int32_t *d_ring_tok = nullptr, *d_ring_exit = nullptr, *d_ring_would = nullptr;
   float* d_ring_conf = nullptr;
   float* d_ring_mass = nullptr;
+  bool fill_lazy = false;  // persistent program: batch the KV fill of consecutive exits
+  int fill_slots = 0;      // exit-layer states one batched fill can take
   bool nucleus = false;   // steps also measure the readout token's nucleus rank (calibration, debug)
   int force_cap = 0;
   int32_t *d_force_tok = nullptr, *d_force_exit = nullptr;
@@ -304,6 +306,7 @@ int run_steps(ee_ctx* c, float tau, int exit_layer, int n, const int32_t* d_forc
   hipError_t e;
   const bool pers = c->persistent && c->nwg_persistent > 0 && c->slot >= 0;
   if (pers) {
+    p.lazy_fill = (c->fill_lazy && c->fill_slots > 1) ? c->fill_slots : 0;
     *c->params_pinned = p;
     const ee::PersistentLaunch L{c->params_pinned, c->slot, c->wbf16, c->nwg_persistent, c->lds, c->stream};
     e = prefill ? ee::launch_prefill_persistent(L, c->pos, n) : ee::launch_decode_persistent(L, c->pos, n);
@@ -580,7 +583,8 @@ int ee_create(const ee_config* cfg, void* hip_stream, ee_ctx** out) {
   c->max_splits = (g.max_seq + ee::kAttnSplit - 1) / ee::kAttnSplit;
   {
     const int64_t pairs = ((A / K) + 1) / 2;
-    const int64_t sizes[9] = {int64_t(H), int64_t(H), int64_t(H), int64_t(A * D), int64_t(A * D),
+    const int64_t sizes[9] = {int64_t(H), int64_t(ee::kMaxPending) * int64_t(H), int64_t(H), int64_t(A * D),
+                              int64_t(A * D),
                               int64_t(F), int64_t(2 * K * D), 8,
                               int64_t(K) * pairs * c->max_splits * int64_t(2 * D + 4)};
     uint64_t** ptrs[9] = {&c->d_h, &c->d_hexit, &c->d_z, &c->d_q, &c->d_o, &c->d_a, &c->d_kvnew, &c->d_dec,
@@ -602,6 +606,7 @@ int ee_create(const ee_config* cfg, void* hip_stream, ee_ctx** out) {
 
   DevParams p = make_params(c, INFINITY, 0);
   c->lds = ee::lds_bytes(p);
+  c->fill_slots = ee::fill_batch_slots(p);
   const int cpl = ee::chunks_per_lane(p, c->wbf16);
   if (cpl > (c->wbf16 ? 4 : 2)) {
     c->err = "hidden too large for the compiled kernels (bf16: H <= 2048, fp32: H <= 512)";
@@ -814,6 +819,14 @@ int ee_set_readout_bias(ee_ctx* c, int32_t exit_layer, const float* b, int32_t o
   if (it == c->readout.end() || !b) return fail(c, EE_EINVAL, "no readout at that layer");
   HIPCHK(c, hipMemcpyAsync(it->second.second, b, sizeof(float) * c->cfg.hidden,
                            on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice, c->stream));
+  return EE_OK;
+}
+
+int ee_set_fill_policy(ee_ctx* c, int32_t policy) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  if (policy != EE_FILL_EAGER && policy != EE_FILL_LAZY) return fail(c, EE_EINVAL, "unknown fill policy");
+  c->fill_lazy = policy == EE_FILL_LAZY;
   return EE_OK;
 }
 

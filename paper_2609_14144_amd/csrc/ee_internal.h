@@ -15,6 +15,7 @@ constexpr int kMaxGroup = 8;           // max query heads per KV head
 constexpr int kMaxHeadDim = 256;
 constexpr int kBarGroups = 8;          // first level of the grid barrier (one per XCD)
 constexpr int kParamSlots = 16;        // persistent-kernel parameter blocks per device
+constexpr int kMaxPending = 8;         // exit-layer states a lazy fill batches at most
 constexpr int kStatFloats = 6;         // a head partial (max, sum, second max, argmax, entropy term, mass ahead)
 
 // Per-layer device pointers, repacked layouts:
@@ -93,7 +94,7 @@ struct DevParams {
   // Activations passed between phases, as tagged words: low 32 bits the fp32
   // value, high 32 bits the tag of the phase that wrote it (one 8-byte store).
   uint64_t* h;                  // [H] residual stream
-  uint64_t* h_exit;             // [H] residual stream at the exit layer
+  uint64_t* h_exit;             // [kMaxPending][H] residual stream at the exit layer (slot 0 unless lazy)
   uint64_t* z;                  // [H] readout output
   uint64_t* q;                  // [A*D]
   uint64_t* o;                  // [A*D]
@@ -115,6 +116,7 @@ struct DevParams {
   float* ring_conf;
   float* ring_mass;             // full-head mass ahead of the readout token (when nucleus)
   int nucleus;                  // the final head also measures the readout token's nucleus rank
+  int lazy_fill;                // persistent kernel: > 1 = lazy fill with that many pending slots
   const int32_t* force_tok;     // may be null
   const int32_t* force_exit;    // may be null
   // debug outputs (device, may be null; only meaningful for single steps)
@@ -150,6 +152,7 @@ hipError_t launch_head_eval(const DevParams& p, int wbf16, const float* d_x, int
 // copy the fp32 values of n tagged words to dst (device)
 hipError_t launch_untag(float* dst, const uint64_t* src, int n, hipStream_t s);
 size_t lds_bytes(const DevParams& p);
+int fill_batch_slots(const DevParams& p);  // exit-layer states one lazy fill can batch
 int chunks_per_lane(const DevParams& p, int wbf16);
 int persistent_max_wgs_per_cu(const DevParams& p, int wbf16, size_t lds);
 

@@ -1444,19 +1444,57 @@ __device__ void phase_fill(const DevParams& p, int pos, int wg, int nwg, float* 
   }
 }
 
-// readout: z = W_r h + b_r; workgroup 0 also keeps h as h_exit.
+// Lazy fill (persistent kernel): the exit-layer states of np exited steps
+// (slots 0..np-1 of h_exit, tags ptag) are projected through every skipped
+// layer's key and value rows at once: each row pair is loaded once and
+// applied to every pending state, with the arithmetic of phase_fill, so the
+// cache entries are the ones an eager fill writes.
+template <typename WT, int CPL>
+__device__ void phase_fill_batch(const DevParams& p, int np, const int* ppos, const uint32_t* ptag, int wg,
+                                 int nwg, float* xs, float* red, const Sync& sy) {
+  const int KD = p.K * p.D;
+  const int total = (p.L - p.exit_layer) * KD;
+  if (wg * kWaves >= total) return;
+  for (int k = 0; k < np; ++k) {
+    const Sync sk{sy.poll, ptag[k], 0u, sy.tout, 0u};
+    rmsnorm_stage(p, p.h_exit + static_cast<int64_t>(k) * p.H, nullptr, p.H, sk, xs + k * p.H, red);
+  }
+  const int nch = p.H / Elem<WT>::N;
+  const int tw = nwg * kWaves;
+  RowBlock<WT, 2, CPL> blk;
+  for (int q = wg * kWaves + wave_id(); q < total; q += tw) {
+    const int l = p.exit_layer + q / KD;
+    const int r0 = p.A * p.D + 2 * (q - (q / KD) * KD);
+    const LayerW lw = p.layers[l];
+    blk.load(static_cast<const WT*>(lw.wqkv), p.H, r0, 2, 0, nch);
+    for (int k = 0; k < np; ++k) {
+      float acc[2];
+      blk.dot_gain(xs + k * p.H, lw.g_attn, 2, 0, nch, acc);
+      wave_sum_n<2>(acc);
+      if ((threadIdx.x & 63) == 0) store_qkv_pair<WT>(p, l, ppos[k], r0, acc[0], acc[1], sy.tout, false);
+    }
+  }
+}
+
+// readout: z = W_r h + b_r; workgroup 0 also keeps h as h_exit (in slot).
 template <typename WT, int CPL>
 __device__ void phase_readout(const DevParams& p, int wg, int nwg, float* xs, RowTask<WT, CPL>& t,
-                              const Sync& sy) {
+                              const Sync& sy, int slot = 0) {
   if (wg == 0) {
+    uint64_t* hx = p.h_exit + static_cast<int64_t>(slot) * p.H;
     for (int i = threadIdx.x; i < p.H; i += kWG)
-      tw_store(p.h_exit + i, tw_val(tw_wait(p, p.h + i, sy.tin, sy.poll)), sy.tout);
+      tw_store(hx + i, tw_val(tw_wait(p, p.h + i, sy.tin, sy.poll)), sy.tout);
   }
   phase_rows<WT, CPL>(p, static_cast<const WT*>(p.ro_w), p.H, p.H, p.h, p.z, p.ro_b, 0, wg, nwg, xs, t, sy);
 }
 
 size_t lds_bytes(const DevParams& p) {
   return static_cast<size_t>(lds_vec_floats(p) + 64) * sizeof(float);
+}
+
+int fill_batch_slots(const DevParams& p) {
+  const int k = lds_vec_floats(p) / p.H;  // normalised exit-layer states staged side by side
+  return k < kMaxPending ? k : kMaxPending;
 }
 
 struct Lds {
@@ -1752,14 +1790,14 @@ EE_PHASE_FN run_down(const DevParams& p, int l, float* smem, Tags& tg) {
   tg.h = E;
 }
 
-EE_PHASE_FN run_readout(const DevParams& p, float* smem, Tags& tg) {
+EE_PHASE_FN run_readout(const DevParams& p, float* smem, Tags& tg, int slot) {
   const int wg = opaque_wg();
   const Lds s = lds_carve(p, smem);
   RowTask<WT, CPL> t;
   t.prefetch(static_cast<const WT*>(p.ro_w), p.H, p.H, wg);
   const uint32_t E = ++tg.ep;
   tl_mark(p, 2 * E);
-  phase_readout<WT, CPL>(p, wg, gridDim.x, s.xs, t, Sync{true, tg.h, 0u, E, 0u});
+  phase_readout<WT, CPL>(p, wg, gridDim.x, s.xs, t, Sync{true, tg.h, 0u, E, 0u}, slot);
   tl_mark(p, 2 * E + 1);
   tg.z = E;
   tg.hx = E;
@@ -1787,6 +1825,16 @@ EE_PHASE_FN run_fill(const DevParams& p, int pos, float* smem, Tags& tg) {
   phase_fill<WT, CPL>(p, pos, wg, gridDim.x, s.xs, s.red, Sync{true, tg.hx, 0u, E, 0u});
   tl_mark(p, 2 * E + 1);
 }
+
+EE_PHASE_FN run_fill_batch(const DevParams& p, int np, const int* ppos, const uint32_t* ptag, float* smem,
+                           Tags& tg) {
+  const int wg = opaque_wg();
+  const Lds s = lds_carve(p, smem);
+  const uint32_t E = ++tg.ep;
+  tl_mark(p, 2 * E);
+  phase_fill_batch<WT, CPL>(p, np, ppos, ptag, wg, gridDim.x, s.xs, s.red, Sync{true, 0u, 0u, E, 0u});
+  tl_mark(p, 2 * E + 1);
+}
 #undef EE_PHASE_FN
 
 template <typename WT, int CPL>
@@ -1812,15 +1860,24 @@ __constant__ DevParams c_params[kParamSlots];
 // loop for the KV fill of the remaining layers. Every step ends with a grid
 // barrier: the next step reads KV rows this step wrote (the fill's included),
 // and with forced tokens nothing else orders the two steps.
+// With the lazy fill an exit only records its position and keeps its
+// exit-layer state in the next h_exit slot; the pending positions are filled
+// together before the first layer above exit_layer runs (then a grid barrier
+// orders the new rows before that layer's attention reads them), when the
+// slots are full, and before the launch ends.
 template <typename WT, int CPL>
 __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_decode_persistent(
     int slot, int pos0, int n, int prefill) {
   extern __shared__ float smem[];
   __shared__ int sh_exited;
+  __shared__ int sh_pend_pos[kMaxPending];
+  __shared__ uint32_t sh_pend_tag[kMaxPending];
   const DevParams& p = c_params[slot];
   Tags tg{};
   uint32_t bep = 0;
   const int Le = p.exit_layer;
+  const bool lazy = !prefill && p.lazy_fill > 1 && Le > 0 && Le < p.L;  // lazy_fill = slots
+  int npend = 0;
   for (int i = 0; i < n; ++i) {
     if (aborted(p)) break;
     const int pos = pos0 + i;
@@ -1828,7 +1885,7 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     for (int l = 0; l < p.L; ++l) {
       run_layer<WT, CPL>(p, l, pos, i, smem, tg);
       if (l + 1 == Le) {
-        run_readout<WT, CPL>(p, smem, tg);
+        run_readout<WT, CPL>(p, smem, tg, lazy ? npend : 0);
         run_head<WT, CPL>(p, 1, i, smem, tg);
         __syncthreads();
         if (threadIdx.x == 0) sh_exited = __float_as_int(tw_val(tw_wait(p, p.dec, tg.gate, true)));
@@ -1838,10 +1895,29 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
           tg.tok = tg.gate;
           break;
         }
+        if (npend > 0) {  // the layers above read the pending positions' rows
+          run_fill_batch<WT, CPL>(p, npend, sh_pend_pos, sh_pend_tag, smem, tg);
+          npend = 0;
+          bar_arrive(p, bep, blockIdx.x, gridDim.x);
+          bar_wait(p, bep);
+        }
       }
     }
     if (exited) {
-      if (Le < p.L) run_fill<WT, CPL>(p, pos, smem, tg);
+      if (lazy) {
+        __syncthreads();
+        if (threadIdx.x == 0) {
+          sh_pend_pos[npend] = pos;
+          sh_pend_tag[npend] = tg.hx;
+        }
+        __syncthreads();
+        if (++npend == p.lazy_fill) {
+          run_fill_batch<WT, CPL>(p, npend, sh_pend_pos, sh_pend_tag, smem, tg);
+          npend = 0;
+        }
+      } else if (Le < p.L) {
+        run_fill<WT, CPL>(p, pos, smem, tg);
+      }
     } else if (!prefill || i == n - 1) {
       run_head<WT, CPL>(p, 0, i, smem, tg);
       tg.tok = tg.ep;
@@ -1849,6 +1925,7 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     bar_arrive(p, bep, blockIdx.x, gridDim.x);
     bar_wait(p, bep);
   }
+  if (npend > 0 && !aborted(p)) run_fill_batch<WT, CPL>(p, npend, sh_pend_pos, sh_pend_tag, smem, tg);
 }
 
 // Launch state of the persistent kernel: barrier and last-arriver counters,

@@ -293,6 +293,48 @@ def test_refresh_recomputes_the_cache(persistent):
             e.ee_refresh(n)
 
 
+def _kv_all(e, cfg, positions):
+    out = []
+    for l in range(cfg.n_layers):
+        for t in positions:
+            k, v = e.ee_read_kv(l, t)
+            out.append(np.concatenate([k, v]))
+    return np.stack(out)
+
+
+@pytest.mark.parametrize("name", ["tiny_bf16", "d1p5b"])
+def test_lazy_fill_is_bit_identical_to_eager(name):
+    """The lazy, batched KV fill writes exactly the cache the eager fill
+    writes and changes nothing else: exit bursts shorter and longer than
+    one batch, a fallback after a burst, and exits still pending when the
+    call returns."""
+    from paper_2609_14144_amd import EE_FILL_LAZY
+    cfg = synth.get_config(name)
+    P = TINY_P if name == "tiny_bf16" else 64
+    Le = 2 if name == "tiny_bf16" else 14
+    fe = np.array([1, 1, 1, 0, 1] + [1] * 10 + [0, 0, 1, 1], np.int32)
+    n = fe.size
+    prompt = synth.prompts(cfg, 1, P)
+    toks = synth.prompts(cfg, 7, n)
+    res = {}
+    for lazy in (False, True):
+        e = engine(name, P + n + 4, True, page_size=16)
+        if lazy:
+            e.ee_set_fill_policy(EE_FILL_LAZY)
+        e.ee_prefill(prompt)
+        res[lazy] = (e.ee_decode_n_ex(0.5, Le, n, force_tokens=toks, force_exit=fe),
+                     _kv_all(e, cfg, range(P, P + n)))
+        if name == "tiny_bf16" and lazy:
+            o = oracle_for(name, P + n + 4)
+            o.prefill(prompt)
+            o.generate(None, 0.5, Le, n, force_tokens=toks, force_exit=fe)
+            check_kv(e, o, cfg, range(cfg.n_layers), range(P, P + n))
+        e.close()
+    for a, b in zip(res[False][0], res[True][0]):
+        np.testing.assert_array_equal(a, b)
+    np.testing.assert_array_equal(res[False][1], res[True][1])
+
+
 def test_error_paths():
     from paper_2609_14144_amd import EEError
     name = "tiny"
