@@ -606,3 +606,99 @@ def test_head_kernel_planted_ties_full_vocab():
             if key == "margin" and layer == 0:
                 assert c2 == 0.0  # the planted tie
         e.ee_set_confidence_measure(0)
+
+
+# ---------------------------------------------------------------------------
+# the other configurations at full size: 0.5B and 3B shapes, the exit-layer
+# sweep of the 1.5B shape, and the long-context run with bursty exits
+# ---------------------------------------------------------------------------
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ["d0p5b", "d3b"])
+def test_other_model_shapes_lockstep(name):
+    """The 0.5B and 3B shapes (readout at half depth): four teacher-forced
+    steps in lockstep with the oracle, alternating imposed branches, after a
+    64-token prompt."""
+    cfg = synth.get_config(name)
+    Le = cfg.readout_layers[0]
+    prompt = synth.prompts(cfg, 1, 64)
+    o = oracle_for(name, 64 + 8)
+    g0 = o.prefill(prompt)
+    e = engine(name, 64 + 8)
+    g = e.ee_prefill(prompt)
+    assert g == g0 or o.last_prefill_stats[2] <= MARGIN
+    rep, outside = lockstep(e, o, g0, 0.3, Le, 4, force_tokens=synth.prompts(cfg, 3, 4),
+                            force_exit=[1, 0, 1, 0])
+    print(name, "worst rel err", max(r for _, r in rep), "outside-margin steps", outside)
+    e.close()
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("Le", [7, 21])
+def test_d1p5b_exit_layer_sweep(Le):
+    """Readouts a quarter and three quarters deep (the exit-layer sweep of the
+    1.5B shape): eight steps in one launch with imposed branches against the
+    oracle, and the skipped layers' cache entries of the exited steps."""
+    name = "d1p5b_sweep"
+    cfg = synth.get_config(name)
+    P = 256
+    prompt = synth.prompts(cfg, 1, P)
+    o = oracle_for(name, P + 16)
+    o.prefill(prompt)
+    toks = synth.prompts(cfg, 8, 8)
+    fe = np.array([1, 0, 1, 1, 0, 0, 1, 0], np.int32)
+    rs = o.generate(None, 0.3, Le, 8, force_tokens=toks, force_exit=fe)
+    e = engine(name, P + 16)
+    e.ee_prefill(prompt)
+    tok, ex, conf, would = e.ee_decode_n_ex(0.3, Le, 8, force_tokens=toks, force_exit=fe)
+    for i, r in enumerate(rs):
+        assert ex[i] == bool(fe[i])
+        assert abs(conf[i] - r.conf) <= 1e-4 + 1e-3 * r.conf
+        if abs(r.conf - 0.3) > MARGIN:
+            assert would[i] == r.would_exit
+        gap = r.gap_readout if r.exited else r.gap_full
+        if gap > MARGIN:
+            assert tok[i] == r.token, i
+    check_kv(e, o, cfg, range(Le, cfg.n_layers, 3), [P + i for i in range(8) if fe[i]])
+    e.close()
+
+
+@pytest.mark.timeout(900)
+def test_d1p5b_long_context_bias_bursts():
+    """Long context (8192-token prompt) with bursts of exits driven through
+    the readout offset, as the long-context configuration does: a step whose
+    offset is beta * e_j (e_j the unit embedding row of token j scaled by
+    sqrt(H), beta = 8 sqrt(H)) exits with token j at confidence ~1; the
+    two device programs agree bit for bit over the whole schedule."""
+    from oracle.numerics import bf16_bits_to_f64
+    cfg = synth.get_config(D15)
+    w = weights_for(D15)
+    P, H = 8192, cfg.hidden
+    prompt = synth.prompts(cfg, 3, P)
+    rng = np.random.default_rng(17)
+    state, sched = 0, []
+    for _ in range(24):  # two-state chain: stay 7/8 in a burst, enter one with 1/2
+        state = int(rng.random() < (7 / 8 if state else 0.5))
+        sched.append(state)
+    targets = rng.integers(0, cfg.vocab, 24)
+    tau = 0.9
+    runs = {}
+    for pers in (True, False):
+        e = engine(D15, P + 32, pers)
+        e.ee_prefill(prompt)
+        out = []
+        for i, (s_on, j) in enumerate(zip(sched, targets)):
+            b = np.zeros(H, np.float32)
+            if s_on:
+                ej = bf16_bits_to_f64(w["embed"][j])
+                b = (8 * math.sqrt(H) * ej / np.linalg.norm(ej) * math.sqrt(H)).astype(np.float32)
+            e.ee_set_readout_bias(14, b)
+            tok, exited, conf = e.ee_decode_step(tau, 14)
+            if s_on:
+                assert exited and tok == j and conf > 0.99, (i, tok, j, conf)
+            else:
+                assert exited == (conf > tau)
+            out.append((tok, exited, conf))
+        runs[pers] = out
+        e.close()
+    assert runs[True] == runs[False]
+    print("long-context schedule exits", sum(x[1] for x in runs[True]), "of", len(sched))
