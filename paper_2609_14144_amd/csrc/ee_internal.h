@@ -7,7 +7,7 @@
 
 namespace ee {
 
-constexpr int kWG = 256;               // threads per workgroup, every kernel
+constexpr int kWG = 512;               // threads per workgroup, every kernel
 constexpr int kWaves = kWG / 64;       // 64-wide wavefronts per workgroup
 constexpr int kPosPerWave = 16;             // attention positions per wave
 constexpr int kAttnSplit = kWaves * kPosPerWave;  // positions per attention work item

@@ -700,5 +700,8 @@ def test_d1p5b_long_context_bias_bursts():
             out.append((tok, exited, conf))
         runs[pers] = out
         e.close()
-    assert runs[True] == runs[False]
+    # tokens and branches identical; the confidence to rounding (the head's
+    # vocabulary partition follows the grid, so its sums round differently)
+    for a, b in zip(runs[True], runs[False]):
+        assert a[:2] == b[:2] and abs(a[2] - b[2]) <= 1e-6, (a, b)
     print("long-context schedule exits", sum(x[1] for x in runs[True]), "of", len(sched))
