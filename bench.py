@@ -146,6 +146,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--fill", choices=["eager", "lazy"], default="eager",
+                    help="KV-absence fill in the exit step, or deferred and batched")
     ap.add_argument("--confidence", choices=list(MEASURES), default="maxprob",
                     help="softmax confidence measure the gate compares with tau (Section 10)")
     ap.add_argument("--copy-probe", type=float, default=0.0, metavar="MIB",
@@ -186,6 +188,7 @@ def main():
     e.ee_load_weights(w)
     e.ee_set_persistent(args.program == "persistent")
     e.ee_set_confidence_measure(MEASURES[args.confidence])
+    e.ee_set_fill_policy(1 if args.fill == "lazy" else 0)
     log("weights resident on the GPU")
 
     cal = [synth.prompts(cfg, 200 + i, PROMPT) for i in range(args.cal_prompts)]
@@ -262,6 +265,7 @@ def main():
             "tau": head["tau"],
             "program": args.program,
             "confidence": args.confidence,
+            "fill": args.fill,
         },
         "roofline": roofline,
         "cpu_baseline": cpu,
