@@ -1059,16 +1059,22 @@ __device__ void phase_rows(const DevParams& p, const WT* W, int rows, int cols, 
 // ---------------------------------------------------------------------------
 constexpr int kRS = 4;  // rows per streamed block
 
+// Gate/up rows per block: two blocks, both requested before the input wait,
+// hold all of a wave's 8-9 rows at the 1.5B shape; wide rows (CPL 4) keep
+// blocks of 4 within the register budget.
+template <int CPL>
+constexpr int gu_rows() { return CPL >= 4 ? 4 : 6; }
+
 __device__ __forceinline__ int gu_begin(const DevParams& p, int gw, int tw) {
   return static_cast<int>(static_cast<int64_t>(p.F) * gw / tw);
 }
 
 template <typename WT, int CPL>
 struct GateUpTask {
-  RowBlock<WT, kRS, CPL> a, b;
-  __device__ __forceinline__ static Tiling<WT, kRS, CPL> tiling(const DevParams& p, int wg, int nwg) {
+  RowBlock<WT, gu_rows<CPL>(), CPL> a, b;
+  __device__ __forceinline__ static Tiling<WT, gu_rows<CPL>(), CPL> tiling(const DevParams& p, int wg, int nwg) {
     const int tw = nwg * kWaves, gw = wg * kWaves + wave_id();
-    return Tiling<WT, kRS, CPL>{2 * gu_begin(p, gw, tw), 2 * gu_begin(p, gw + 1, tw), 0,
+    return Tiling<WT, gu_rows<CPL>(), CPL>{2 * gu_begin(p, gw, tw), 2 * gu_begin(p, gw + 1, tw), 0,
                                 p.H / Elem<WT>::N, 1};
   }
   __device__ __forceinline__ void prefetch(const DevParams& p, int l, int wg, int nwg) {
@@ -1090,11 +1096,11 @@ __device__ void phase_gateup(const DevParams& p, int l, int wg, int nwg, float* 
   const LayerW lw = p.layers[l];
   rmsnorm_stage(p, p.h, lw.g_mlp, p.H, sy, xs, red);
   uint64_t* a_out = p.a;
-  stream_tiles<WT, kRS, CPL>(static_cast<const WT*>(lw.wgu), p.H, GateUpTask<WT, CPL>::tiling(p, wg, nwg),
-                             xs, t.a, t.b, [&](int r0, int nr, const float(&acc)[kRS]) {
+  stream_tiles<WT, gu_rows<CPL>(), CPL>(static_cast<const WT*>(lw.wgu), p.H, GateUpTask<WT, CPL>::tiling(p, wg, nwg),
+                             xs, t.a, t.b, [&](int r0, int nr, const float(&acc)[gu_rows<CPL>()]) {
                               if ((threadIdx.x & 63) == 0) {
 #pragma unroll
-                                for (int i = 0; i < kRS / 2; ++i)
+                                for (int i = 0; i < gu_rows<CPL>() / 2; ++i)
                                   if (2 * i < nr) tw_store(a_out + r0 / 2 + i, silu(acc[2 * i]) * acc[2 * i + 1], sy.tout);
                               }
                             }, 2);
