@@ -658,6 +658,25 @@ __device__ __forceinline__ void keep_packed(uint4& x) {
 
 // reductions over the PPW row groups of a wave (one value per group, read
 // from the group's first lane); every lane gets the same result
+// v summed over the lanes that share lane % LPP (LPP = 8 or 16): lane l gets
+// the sum over l ^ 8 (LPP 8), l ^ 16 and l ^ 32 without LDS: a DPP rotate by
+// 8 within 16-lane rows, then the gfx950 cross-row swaps. Every lane adds
+// the same two values at each step, so all lanes hold the same bits.
+__device__ __forceinline__ float add_swapped16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float add_swapped32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+template <int LPP>
+__device__ __forceinline__ float sum_lanes_xor(float v) {
+  static_assert(LPP == 8 || LPP == 16, "8 or 16 lanes per position");
+  if constexpr (LPP == 8) v += dpp<0x128>(v);  // row_ror:8 = lane ^ 8 within the row
+  return add_swapped32(add_swapped16(v));
+}
+
 template <int LPP>
 __device__ __forceinline__ float groups_max(float v) {
   float m = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
@@ -868,12 +887,9 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
       }
     }
 #pragma unroll
-    for (int off = LPP; off < 64; off <<= 1) {
-#pragma unroll
-      for (int e = 0; e < N; ++e) {
-        aa[e] += __shfl_xor(aa[e], off, 64);
-        ab[e] += __shfl_xor(ab[e], off, 64);
-      }
+    for (int e = 0; e < N; ++e) {
+      aa[e] = sum_lanes_xor<LPP>(aa[e]);
+      ab[e] = sum_lanes_xor<LPP>(ab[e]);
     }
     if (sub == 0) {
 #pragma unroll
