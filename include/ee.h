@@ -28,9 +28,11 @@
  *     value 0 selects the plain ungated model (no readout, no gate): the
  *     baseline.
  *   - The gate exits iff conf > tau, compared in fp32. tau = +inf never exits;
- *     tau <= 0 always exits (conf >= 1/V > 0). tau = NaN is EE_EINVAL.
- *   - conf is the readout's max softmax probability, also on fallback steps;
- *     for the ungated model it is the full head's.
+ *     under the default measure tau <= 0 always exits (conf >= 1/V > 0).
+ *     tau = NaN is EE_EINVAL.
+ *   - conf is the readout's confidence under the selected measure (its max
+ *     softmax probability unless ee_set_confidence_measure chose another),
+ *     also on fallback steps; for the ungated model it is the full head's.
  *   - Argmax ties go to the lowest token id.
  */
 #ifndef EE_H
@@ -119,8 +121,8 @@ typedef struct ee_debug {
   int32_t would_exit;     /* gate decision (conf > tau) before forcing */
   int32_t readout_token;  /* readout argmax, -1 when ungated */
   int32_t full_token;     /* full-head argmax, -1 when the upper layers were skipped */
-  float conf;             /* readout max-probability (full head's when ungated) */
-  float conf_full;        /* full head max-probability, NaN when skipped */
+  float conf;             /* readout confidence, selected measure (full head's when ungated) */
+  float conf_full;        /* full head confidence, selected measure; NaN when skipped */
   float nucleus_mass;     /* full-head probability ahead of readout_token (order: probability
                              desc, id asc); readout_token is inside the 0.9 nucleus iff this
                              is < 0.9. NaN when skipped or ungated */
