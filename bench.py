@@ -27,6 +27,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "batch-1 decode tokens/sec at exit rate r; achieved HBM GB/s vs peak"
 PEAK_HBM_GBS = 8000.0
+SHAPE_NAMES = {"d1p5b": "1.5B-shaped", "d1p5b_sweep": "1.5B-shaped", "d0p5b": "0.5B-shaped",
+               "d3b": "3B-shaped", "tiny": "tiny", "tiny_bf16": "tiny"}
 MEASURES = {"maxprob": 0, "margin": 1, "negentropy": 2}  # EE_CONF_* of include/ee.h
 PROMPT = 512
 
@@ -254,9 +256,9 @@ def main():
         "dtype": "bf16 weights, f32 accumulate",
         "data": "synthetic (seeded random weights N(0,0.02) and uniform random prompts)",
         "config": {
-            "workload": (f"1.5B-shaped decoder: {cfg.n_layers} layers, H={cfg.hidden}, "
+            "workload": (f"{SHAPE_NAMES.get(cfg.name, cfg.name)} decoder: {cfg.n_layers} layers, H={cfg.hidden}, "
                          f"{cfg.n_q_heads}/{cfg.n_kv_heads} heads of {cfg.head_dim}, F={cfg.ffn}, "
-                         f"V={cfg.vocab}, bf16; readout at layer {Le}; {PROMPT}-token prompt, "
+                         f"V={cfg.vocab}, {cfg.wdtype}; readout at layer {Le}; {PROMPT}-token prompt, "
                          f"{args.warmup} warm-up + {args.steps} timed decode steps, batch 1; tau "
                          f"calibrated on the GPU to target exit rate 0.5"),
             "exit_layer": Le,
