@@ -225,6 +225,10 @@ def main():
                             "full_depth_steps_equivalent": 16}
     log(f"refresh of 16 positions: {results['refresh16']}")
 
+    # streaming-read ceiling: a plain coalesced 16-byte read of 2 GiB
+    ceiling = e.ee_stream_probe(2 << 30, 5)
+    log(f"streaming-read ceiling: {ceiling:.0f} GB/s")
+
     kname = "k_decode_persistent" if args.program == "persistent" else "per_op"
     per_launch = head["algorithmic_bytes"]
     traffic = None
@@ -234,7 +238,10 @@ def main():
     roofline = {"bound": "hbm", "achieved": head["achieved_GBs"], "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": head["achieved_GBs"] / PEAK_HBM_GBS, "traffic": traffic,
                 "kernel": kname, "algorithmic_bytes_per_launch": per_launch,
-                "launch_ms": head["kernel_ms"]}
+                "launch_ms": head["kernel_ms"],
+                "ceiling": {"GBs": ceiling, "bytes": 2 << 30,
+                            "probe": "k_stream_read: plain 16-byte coalesced reads of 2 GiB, median of 5"},
+                "frac_of_ceiling": head["achieved_GBs"] / ceiling}
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -269,6 +269,18 @@ int ee_set_persistent_grid(ee_ctx* ctx, int32_t nwg);
 int ee_set_timeline(ee_ctx* ctx, int32_t capacity);
 int ee_read_timeline(ee_ctx* ctx, uint64_t* out, int32_t n);
 
+/* Streaming-read ceiling of the device: a plain kernel reads `bytes` (rounded
+ * down to 16-byte words) of a buffer the call allocates and frees, with
+ * 16-byte coalesced loads, each workgroup (eight per compute unit) streaming
+ * one contiguous range; one warm-up launch, then
+ * `reps` timed launches on the context's stream (HIP events). *out_gbps =
+ * bytes / median launch time, in 1e9 B/s. The decode path's achieved bandwidth
+ * is reported against this ceiling as well as against the spec-sheet peak.
+ * Measurement tool, not part of decoding.
+ * Errors: EE_EINVAL (bytes < 16, reps < 1, out_gbps NULL), EE_ENOMEM,
+ * EE_EHIP. */
+int ee_stream_probe(ee_ctx* ctx, int64_t bytes, int32_t reps, float* out_gbps);
+
 /* Device time in milliseconds of the most recent ee_decode_n/_ex call's
  * kernels, measured with HIP events on the context's stream. */
 int ee_last_decode_ms(ee_ctx* ctx, float* out_ms);

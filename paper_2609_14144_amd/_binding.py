@@ -82,6 +82,7 @@ def _load():
         "ee_set_persistent": (C.c_int, [V, C.c_int32]),
         "ee_set_persistent_grid": (C.c_int, [V, C.c_int32]),
         "ee_last_decode_ms": (C.c_int, [V, _FP]),
+        "ee_stream_probe": (C.c_int, [V, C.c_int64, C.c_int32, _FP]),
         "ee_set_timeline": (C.c_int, [V, C.c_int32]),
         "ee_read_timeline": (C.c_int, [V, C.POINTER(C.c_uint64), C.c_int32]),
         "ee_position": (C.c_int32, [V]),
@@ -271,6 +272,12 @@ class Engine:
         ms = C.c_float()
         self._check(lib.ee_last_decode_ms(self._ctx, C.byref(ms)))
         return ms.value
+
+    def ee_stream_probe(self, nbytes: int, reps: int = 5) -> float:
+        """Streaming-read ceiling of the device in 1e9 B/s (median of reps launches)."""
+        gbps = C.c_float()
+        self._check(lib.ee_stream_probe(self._ctx, int(nbytes), int(reps), C.byref(gbps)))
+        return gbps.value
 
     def ee_position(self) -> int:
         return lib.ee_position(self._ctx)

@@ -18,6 +18,10 @@
 
 using ee::DevParams;
 
+namespace ee {
+hipError_t launch_stream_read(const void* p, int64_t n, int n_cu, uint32_t* sink, hipStream_t s);  // ee_probe.hip
+}
+
 struct ee_ctx {
   ee_config cfg{};
   int wbf16 = 0;
@@ -827,6 +831,39 @@ int ee_set_fill_policy(ee_ctx* c, int32_t policy) {
   c->err.clear();
   if (policy != EE_FILL_EAGER && policy != EE_FILL_LAZY) return fail(c, EE_EINVAL, "unknown fill policy");
   c->fill_lazy = policy == EE_FILL_LAZY;
+  return EE_OK;
+}
+
+int ee_stream_probe(ee_ctx* c, int64_t bytes, int32_t reps, float* out_gbps) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  if (!out_gbps || bytes < 16 || reps < 1) return fail(c, EE_EINVAL, "stream probe: bytes >= 16, reps >= 1, output");
+  const int64_t n = bytes / 16;
+  void* buf = nullptr;
+  uint32_t* sink = nullptr;
+  int r;
+  if ((r = dalloc(c, &buf, static_cast<size_t>(n) * 16))) return r;
+  if ((r = dalloc(c, reinterpret_cast<void**>(&sink), 4))) {
+    dfree(buf);
+    return r;
+  }
+  std::vector<float> ms;
+  hipError_t he = hipMemsetAsync(buf, 0, static_cast<size_t>(n) * 16, c->stream);
+  for (int i = 0; i <= reps && he == hipSuccess; ++i) {  // launch 0 warms up
+    if ((he = hipEventRecord(c->ev0, c->stream)) != hipSuccess) break;
+    if ((he = ee::launch_stream_read(buf, n, c->n_cu, sink, c->stream)) != hipSuccess) break;
+    if ((he = hipEventRecord(c->ev1, c->stream)) != hipSuccess) break;
+    if ((he = hipEventSynchronize(c->ev1)) != hipSuccess) break;
+    float t = 0.f;
+    if ((he = hipEventElapsedTime(&t, c->ev0, c->ev1)) != hipSuccess) break;
+    if (i > 0) ms.push_back(t);
+  }
+  dfree(buf);
+  dfree(sink);
+  if (he != hipSuccess) return hip_fail(c, he, "stream probe");
+  std::sort(ms.begin(), ms.end());
+  const float med = ms[ms.size() / 2];
+  *out_gbps = static_cast<float>(static_cast<double>(n) * 16.0 / (med * 1e-3) / 1e9);
   return EE_OK;
 }
 

@@ -98,6 +98,16 @@ def trace(args):
             f"{rf['achieved']:.1f} GB/s of {rf['peak']:.0f} GB/s (frac {rf['frac']:.4f}) from "
             f"{rf['algorithmic_bytes_per_launch'] / 1e9:.3f} GB of algorithmic bytes per launch "
             f"over {rf['launch_ms']:.3f} ms."]
+    ceil = rf.get("ceiling")
+    if ceil:
+        probe = [r for r in stats if "k_stream_read" in r["Name"]]
+        line = (f"Streaming-read ceiling (bench JSON, {ceil['probe']}): {ceil['GBs']:.0f} GB/s; "
+                f"achieved / ceiling = {rf['frac_of_ceiling']:.3f}.")
+        if probe:
+            avg_us = float(probe[0]["AverageNs"]) / 1e3
+            line += (f" The profiler's average for k_stream_read ({probe[0]['Calls']} calls) is "
+                     f"{avg_us:.1f} us per {ceil['bytes'] / 2 ** 30:.0f} GiB = {ceil['bytes'] / avg_us / 1e3:.0f} GB/s.")
+        out += ["", line]
     print("\n".join(out))
 
 

@@ -705,3 +705,15 @@ def test_d1p5b_long_context_bias_bursts():
     for a, b in zip(runs[True], runs[False]):
         assert a[:2] == b[:2] and abs(a[2] - b[2]) <= 1e-6, (a, b)
     print("long-context schedule exits", sum(x[1] for x in runs[True]), "of", len(sched))
+
+
+def test_stream_probe_reads_below_the_hbm_peak():
+    """The streaming-read ceiling of a buffer four times the 256 MB last-level
+    cache comes from HBM: positive and below MI355X's 8 TB/s peak."""
+    from paper_2609_14144_amd import EEError
+    e = engine("tiny", 24)
+    gbps = e.ee_stream_probe(1 << 30, 3)
+    assert 1000.0 < gbps < 8000.0 * 1.02, gbps
+    with pytest.raises(EEError) as ei:
+        e.ee_stream_probe(8, 1)
+    assert ei.value.code == -1
