@@ -548,7 +548,13 @@ __device__ inline int step_token(const DevParams& p, int step, const Sync& sy) {
   return tok;
 }
 
-__device__ __forceinline__ int wave_id() { return static_cast<int>(threadIdx.x >> 6); }
+// The wave's index in the workgroup, as a wave-uniform (scalar) value: the
+// row ranges, tile counts and loop bounds derived from it then live in scalar
+// registers and branch on scalar conditions, instead of per-lane values whose
+// loops and conditional tile loads compile to exec-mask sequences.
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+}
 
 // ---------------------------------------------------------------------------
 // phase: RMSNorm + QKV projection + RoPE + KV append (one layer). Global wave
