@@ -70,18 +70,30 @@ def measured_traffic(kernel, n_steps_expected):
     return rec
 
 
-def run_condition(e, cfg, tau, exit_layer, prompt, warmup, steps):
+def run_condition(e, cfg, tau, exit_layer, prompt, warmup, steps, full_every=None):
+    """full_every: None = the gate decides; k >= 1 = a fixed schedule that
+    runs the full network on every k-th step and exits on the others
+    (Section 7's schedules; k = 0: exit on every step)."""
+    import numpy as np
     import torch
     e.ee_reset()
     e.ee_prefill(prompt)
+
+    def decode(n):
+        if full_every is None:
+            return e.ee_decode_n(tau, exit_layer, n)
+        sched = np.ones(n, np.int32) if full_every == 0 else (np.arange(n) % full_every != 0).astype(np.int32)
+        tok, ex, conf, _ = e.ee_decode_n_ex(tau, exit_layer, n, force_exit=sched)
+        return tok, ex, conf
+
     if warmup:
-        e.ee_decode_n(tau, exit_layer, warmup)
+        decode(warmup)
     pos0 = e.ee_position()
     # a one-element kernel that marks the timed launch in profiler traces
     torch.sigmoid(torch.zeros(1, device="cuda"))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    tok, ex, conf = e.ee_decode_n(tau, exit_layer, steps)
+    tok, ex, conf = decode(steps)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     kernel_ms = e.ee_last_decode_ms()
@@ -214,6 +226,11 @@ def main():
     if not args.no_sweep:
         results["ungated"] = run_condition(e, cfg, math.inf, 0, prompt, args.warmup, args.steps)
         log(f"ungated: {results['ungated']}")
+        # Section 7's fixed schedules, by cost: every step from the readout,
+        # and the full network on every 2nd / 4th step regardless of confidence
+        for name, k in (("always_exit", 0), ("full_every_2nd", 2), ("full_every_4th", 4)):
+            results[name] = run_condition(e, cfg, math.inf, Le, prompt, args.warmup, args.steps, full_every=k)
+            log(f"{name}: {results[name]}")
     head = results["r0.5"]
     # periodic full-depth refresh (Section 10) of the 16 most recent positions,
     # after the last timed run: one launch of 16 full-depth steps
