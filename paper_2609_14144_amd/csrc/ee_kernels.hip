@@ -634,6 +634,12 @@ __device__ void phase_qkv(const DevParams& p, int l, int pos, int step, int wg, 
 // input; only the row of position pos, written by the projection phase, is
 // read after it (from its tagged copy).
 // ---------------------------------------------------------------------------
+// e^x as 2^(x log2 e) on the hardware base-2 exponential (v_exp_f32): within
+// a few ulps, against a dozen instructions of the library routine's range
+// reduction. Used on the attention softmax (arguments are scores minus their
+// running maximum, <= 0; exp(-inf) = 0 for padded rows) and in SiLU.
+__device__ __forceinline__ float fexp(float x) { return __builtin_amdgcn_exp2f(x * 1.44269504088896341f); }
+
 __host__ __device__ inline int attn_nsplit(int pos) { return (pos + kAttnSplit) / kAttnSplit; }
 __host__ __device__ inline int attn_pairs(int G) { return (G + 1) >> 1; }
 __host__ __device__ inline int attn_wave_floats(int D) {
@@ -870,8 +876,8 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
     float la = 0.f, lb = 0.f;
 #pragma unroll
     for (int k = 0; k < RPL; ++k) {
-      sa[k] = expf(sa[k] - ma);  // exp(-inf) = 0 for rows past the wave's end
-      sb[k] = expf(sb[k] - mb);
+      sa[k] = fexp(sa[k] - ma);  // exp(-inf) = 0 for rows past the wave's end
+      sb[k] = fexp(sb[k] - mb);
       la += sa[k];
       lb += sb[k];
     }
@@ -929,7 +935,7 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
     for (int w = 0; w < kWaves; ++w) {
       if (w < nw) {
         const float* wb2 = lds + 2 * D + w * WF + 2 * kPosPerWave;
-        const float f = expf(mw[w] - M);
+        const float f = fexp(mw[w] - M);
         den = fmaf(f, wb2[2 * D + 2 + hg], den);
         num = fmaf(f, act ? wb2[tid] : 0.f, num);
       }
@@ -989,10 +995,10 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
     if (act && dd == 0) {
       float cm = Mr;
       for (int s2 = 0; s2 < ns; ++s2) cm = fmaxf(cm, rl[s2 * RS + 2 * D + hg]);
-      const float sc = expf(Mr - cm);  // 0 while nothing has been merged yet
+      const float sc = fexp(Mr - cm);  // 0 while nothing has been merged yet
       float dn = Dr * sc;
       for (int s2 = 0; s2 < ns; ++s2) {
-        const float f = expf(rl[s2 * RS + 2 * D + hg] - cm);
+        const float f = fexp(rl[s2 * RS + 2 * D + hg] - cm);
         wts[s2 * 2 + hg] = f;
         dn = fmaf(f, rl[s2 * RS + 2 * D + 2 + hg], dn);
       }
@@ -1107,7 +1113,7 @@ struct GateUpTask {
   }
 };
 
-__device__ inline float silu(float x) { return x / (1.f + expf(-x)); }
+__device__ inline float silu(float x) { return x / (1.f + fexp(-x)); }
 
 template <typename WT, int CPL>
 __device__ void phase_gateup(const DevParams& p, int l, int wg, int nwg, float* xs, float* red,
