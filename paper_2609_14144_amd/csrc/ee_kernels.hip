@@ -637,7 +637,8 @@ __device__ void phase_qkv(const DevParams& p, int l, int pos, int step, int wg, 
 // e^x as 2^(x log2 e) on the hardware base-2 exponential (v_exp_f32): within
 // a few ulps, against a dozen instructions of the library routine's range
 // reduction. Used on the attention softmax (arguments are scores minus their
-// running maximum, <= 0; exp(-inf) = 0 for padded rows) and in SiLU.
+// running maximum, <= 0; exp(-inf) = 0 for padded rows), in SiLU and in the
+// vocabulary head's online softmax statistics.
 __device__ __forceinline__ float fexp(float x) { return __builtin_amdgcn_exp2f(x * 1.44269504088896341f); }
 
 __host__ __device__ inline int attn_nsplit(int pos) { return (pos + kAttnSplit) / kAttnSplit; }
@@ -1225,7 +1226,7 @@ __device__ inline Stat stat_empty() { return Stat{-INFINITY, 0.f, -INFINITY, 0x7
 // logit and lower id)
 __device__ inline void stat_push(Stat& st, float v, int r, bool ahead) {
   if (v > st.m) {
-    const float sc = expf(st.m - v);
+    const float sc = fexp(st.m - v);
     st.t = st.s > 0.f ? sc * (st.t + (st.m - v) * st.s) : 0.f;
     st.a = st.a * sc + (ahead ? 1.f : 0.f);
     st.s = st.s * sc + 1.f;
@@ -1233,7 +1234,7 @@ __device__ inline void stat_push(Stat& st, float v, int r, bool ahead) {
     st.m = v;
     st.idx = r;
   } else {
-    const float e = expf(v - st.m);
+    const float e = fexp(v - st.m);
     st.s += e;
     st.t = fmaf(e, v - st.m, st.t);
     if (ahead) st.a += e;
@@ -1247,7 +1248,7 @@ __device__ inline Stat stat_merge(Stat a, Stat b) {
   const bool bw = b.m > a.m || (b.m == a.m && b.idx < a.idx);
   Stat w = bw ? b : a;
   const Stat o = bw ? a : b;
-  const float sc = expf(o.m - w.m);
+  const float sc = fexp(o.m - w.m);
   w.t = w.t + sc * (o.t + (o.m - w.m) * o.s);
   w.a = w.a + o.a * sc;
   w.s = w.s + o.s * sc;
