@@ -328,16 +328,30 @@ __device__ inline void stage_coh(const float* x, int n, float* xs) {
 }
 
 // xs[i] = x[i] * rsqrt(mean(x^2) + eps) * (g ? g[i] : 1), x tagged words
+// The gains of the thread's first kGR elements are requested before the
+// input wait, so no global round trip follows it.
 template <int kB = 8>
 __device__ inline void rmsnorm_stage(const DevParams& p, const uint64_t* x, const float* __restrict__ g,
                                      int n, const Sync& sy, float* xs, float* red) {
+  constexpr int kGR = 4;
+  float gr[kGR];
+#pragma unroll
+  for (int j = 0; j < kGR; ++j) {
+    const int i = static_cast<int>(threadIdx.x) + j * kWG;
+    gr[j] = (g && i < n) ? g[i] : 1.f;
+  }
   __syncthreads();  // xs may still be read by a previous phase
   tw_stage<kB>(p, x, n, sy.tin, sy.poll, xs);
   __syncthreads();
   float ss = 0.f;
   for (int i = threadIdx.x; i < n; i += kWG) ss = fmaf(xs[i], xs[i], ss);
   const float r = rsqrtf(block_sum(ss, red) / static_cast<float>(n) + p.eps);
-  for (int i = threadIdx.x; i < n; i += kWG) xs[i] = xs[i] * r * (g ? g[i] : 1.f);
+#pragma unroll
+  for (int j = 0; j < kGR; ++j) {
+    const int i = static_cast<int>(threadIdx.x) + j * kWG;
+    if (i < n) xs[i] = xs[i] * r * gr[j];
+  }
+  for (int i = static_cast<int>(threadIdx.x) + kGR * kWG; i < n; i += kWG) xs[i] = xs[i] * r * (g ? g[i] : 1.f);
   __syncthreads();
 }
 
