@@ -513,23 +513,43 @@ __device__ inline int64_t kv_offset(const DevParams& p, int l, int pos, int kvh)
 // consecutive elements. q goes to its tagged vector; k and v go to the cache
 // and, when kvnew is set, also (storage-rounded) to the tagged copy of this
 // step's row that the attention phase reads.
+// What the store of row pair r0 reads from global memory (the rotation of
+// its RoPE pair, its cache row), gathered before the phase waits for its
+// input so that no load round trip follows the dot product.
+struct QkvPre {
+  float c, s;    // cos / sin of the pair's angle at pos (q and k rows)
+  int64_t off;   // cache offset of the row's (layer, position, kv head) (k and v rows)
+};
+
+__device__ inline QkvPre qkv_pre(const DevParams& p, int l, int pos, int r0) {
+  const int AD = p.A * p.D, KD = p.K * p.D;
+  QkvPre q{1.f, 0.f, 0};
+  if (r0 < AD + KD) {
+    const int head = r0 / p.D, rl = r0 - head * p.D, half = p.D >> 1;
+    q.c = p.rope_cos[static_cast<int64_t>(pos) * half + (rl >> 1)];
+    q.s = p.rope_sin[static_cast<int64_t>(pos) * half + (rl >> 1)];
+    if (r0 >= AD) q.off = kv_offset(p, l, pos, head - p.A);
+  } else {
+    q.off = kv_offset(p, l, pos, (r0 - AD - KD) / p.D);
+  }
+  return q;
+}
+
 template <typename WT>
-__device__ inline void store_qkv_pair(const DevParams& p, int l, int pos, int r0, float x1, float x2,
+__device__ inline void store_qkv_pair(const DevParams& p, const QkvPre& pre, int r0, float x1, float x2,
                                       uint32_t tag, bool kvnew) {
   const int AD = p.A * p.D, KD = p.K * p.D;
   if (r0 < AD + KD) {
     const int head = r0 / p.D;
     const int rl = r0 - head * p.D;  // = 2i
-    const int half = p.D >> 1;
-    const float c = p.rope_cos[static_cast<int64_t>(pos) * half + (rl >> 1)];
-    const float s = p.rope_sin[static_cast<int64_t>(pos) * half + (rl >> 1)];
+    const float c = pre.c, s = pre.s;
     const float y1 = x1 * c - x2 * s;
     const float y2 = x2 * c + x1 * s;
     if (r0 < AD) {
       tw_store(p.q + r0, y1, tag);
       tw_store(p.q + r0 + 1, y2, tag);
     } else {
-      WT* kp = static_cast<WT*>(p.kpool) + kv_offset(p, l, pos, head - p.A) + rl;
+      WT* kp = static_cast<WT*>(p.kpool) + pre.off + rl;
       Elem<WT>::store_pair(kp, y1, y2);
       if (kvnew) {
         tw_store(p.kvnew + (r0 - AD), Elem<WT>::round(y1), tag);
@@ -538,8 +558,8 @@ __device__ inline void store_qkv_pair(const DevParams& p, int l, int pos, int r0
     }
   } else {
     const int j = r0 - AD - KD;
-    const int kvh = j / p.D, d = j - kvh * p.D;
-    WT* vp = static_cast<WT*>(p.vpool) + kv_offset(p, l, pos, kvh) + d;
+    const int d = j - (j / p.D) * p.D;
+    WT* vp = static_cast<WT*>(p.vpool) + pre.off + d;
     Elem<WT>::store_pair(vp, x1, x2);
     if (kvnew) {
       tw_store(p.kvnew + KD + j, Elem<WT>::round(x1), tag);
@@ -579,8 +599,10 @@ __device__ __forceinline__ int wave_id() {
 template <typename WT, int CPL>
 struct QkvTask {
   RowBlock<WT, 2, CPL> blk;
-  __device__ __forceinline__ void prefetch(const DevParams& p, int l, int wg) {
+  QkvPre pre;  // of the wave's first pair
+  __device__ __forceinline__ void prefetch(const DevParams& p, int l, int pos, int wg) {
     const int pair = wg * kWaves + wave_id();
+    if ((threadIdx.x & 63) == 0 && pair < (p.qkv_rows >> 1)) pre = qkv_pre(p, l, pos, 2 * pair);
     blk.load(static_cast<const WT*>(p.layers[l].wqkv), p.H, 2 * pair, pair < (p.qkv_rows >> 1) ? 2 : 0,
              0, p.H / Elem<WT>::N);
   }
@@ -621,7 +643,9 @@ __device__ void phase_qkv(const DevParams& p, int l, int pos, int step, int wg, 
     float acc[2];
     t.blk.dot(xs, 2, 0, nch, acc);
     wave_sum_n<2>(acc);
-    if ((threadIdx.x & 63) == 0) store_qkv_pair<WT>(p, l, pos, 2 * pair, acc[0], acc[1], sy.tout, true);
+    if ((threadIdx.x & 63) == 0)
+      store_qkv_pair<WT>(p, pair == wg * kWaves + wave_id() ? t.pre : qkv_pre(p, l, pos, 2 * pair), 2 * pair, acc[0],
+                         acc[1], sy.tout, true);
   }
 }
 
@@ -1079,6 +1103,7 @@ __device__ void phase_rows(const DevParams& p, const WT* W, int rows, int cols, 
   // the residual of the wave's first row is read before the input is staged
   float prev0 = 0.f;
   if (residual && (threadIdx.x & 63) == 0 && r0 < rows) prev0 = tw_val(tw_wait(p, out + r0, sy.tres, sy.poll));
+  else if (bias && (threadIdx.x & 63) == 0 && r0 < rows) prev0 = bias[r0];  // requested before the input wait
   copy_stage(p, x, cols, sy, xs);
   const int nch = cols / Elem<WT>::N;
   const int tw = nwg * kWaves;
@@ -1088,8 +1113,8 @@ __device__ void phase_rows(const DevParams& p, const WT* W, int rows, int cols, 
     t.blk.dot(xs, 1, 0, nch, acc);
     acc[0] = wave_sum(acc[0]);
     if ((threadIdx.x & 63) == 0) {
-      float prev = bias ? bias[r] : 0.f;
-      if (residual) prev = r == r0 ? prev0 : tw_val(tw_wait(p, out + r, sy.tres, sy.poll));
+      float prev = r == r0 ? prev0 : (bias ? bias[r] : 0.f);
+      if (residual && r != r0) prev = tw_val(tw_wait(p, out + r, sy.tres, sy.poll));
       tw_store(out + r, prev + acc[0], sy.tout);
     }
   }
@@ -1489,7 +1514,7 @@ __device__ void phase_fill(const DevParams& p, int pos, int wg, int nwg, float* 
     float acc[2];
     blk.dot_gain(xs, lw.g_attn, 2, 0, nch, acc);
     wave_sum_n<2>(acc);
-    if ((threadIdx.x & 63) == 0) store_qkv_pair<WT>(p, l, pos, r0, acc[0], acc[1], sy.tout, false);
+    if ((threadIdx.x & 63) == 0) store_qkv_pair<WT>(p, qkv_pre(p, l, pos, r0), r0, acc[0], acc[1], sy.tout, false);
   }
 }
 
@@ -1520,7 +1545,8 @@ __device__ void phase_fill_batch(const DevParams& p, int np, const int* ppos, co
       float acc[2];
       blk.dot_gain(xs + k * p.H, lw.g_attn, 2, 0, nch, acc);
       wave_sum_n<2>(acc);
-      if ((threadIdx.x & 63) == 0) store_qkv_pair<WT>(p, l, ppos[k], r0, acc[0], acc[1], sy.tout, false);
+      if ((threadIdx.x & 63) == 0)
+        store_qkv_pair<WT>(p, qkv_pre(p, l, ppos[k], r0), r0, acc[0], acc[1], sy.tout, false);
     }
   }
 }
@@ -1571,7 +1597,7 @@ __global__ __launch_bounds__(kWG) void k_op(DevParams p, int l, int pos, int ste
   const Sync sy{false, 0u, 0u, 0u, 0u};  // kernel boundaries order the operations
   if constexpr (OP == kOpQkv) {
     QkvTask<WT, CPL> t;
-    t.prefetch(p, l, wg);
+    t.prefetch(p, l, pos, wg);
     phase_qkv<WT, CPL>(p, l, pos, step, wg, nwg, s.xs, s.red, t, sy);
   }
   if constexpr (OP == kOpAttn) {
@@ -1768,7 +1794,7 @@ EE_PHASE_FN run_qkv(const DevParams& p, int l, int pos, int step, float* smem, T
   const int wg = opaque_wg();
   const Lds s = lds_carve(p, smem);
   QkvTask<WT, CPL> t;
-  t.prefetch(p, l, wg);
+  t.prefetch(p, l, pos, wg);
   const uint32_t E = ++tg.ep;
   tl_mark(p, 2 * E);
   phase_qkv<WT, CPL>(p, l, pos, step, wg, gridDim.x, s.xs, s.red, t, Sync{true, tg.h, tg.tok, E, 0u});
