@@ -56,9 +56,10 @@ def step_bytes(cfg, exit_layer, T, exited, gated):
     return L * (layer + kv_read + kv_write) + readout + 2 * E
 
 
-def measured_traffic(kernel, n_steps_expected):
-    """HBM bytes per launch from committed rocprofv3 counter summaries, if
-    they were taken on the current kernel source; else None."""
+def measured_traffic(kernel, steps, warmup, prompt_len):
+    """HBM bytes of the headline launch from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel source and on a launch of
+    the same shape (steps, warm-up, prompt) as this run's; else None."""
     path = os.path.join(ROOT, "profiles", f"{kernel}_traffic.json")
     if not os.path.exists(path):
         return None
@@ -67,17 +68,19 @@ def measured_traffic(kernel, n_steps_expected):
     from paper_2609_14144_amd.rocprof_summary import kernel_source_hash
     if rec.get("kernel_source_hash") != kernel_source_hash():
         return None
+    if (rec.get("steps"), rec.get("warmup"), rec.get("prompt")) != (steps, warmup, prompt_len):
+        return None
     return rec
 
 
-def run_condition(e, cfg, tau, exit_layer, prompt, warmup, steps, full_every=None):
-    """full_every: None = the gate decides; k >= 1 = a fixed schedule that
-    runs the full network on every k-th step and exits on the others
+def run_condition(e, cfg, tau, exit_layer, prompt, warmup, steps, full_every=None, reps=3):
+    """One condition, timed `reps` times from the same state (reset, prompt,
+    warm-up, then one timed launch of `steps` steps); the median launch is
+    reported. full_every: None = the gate decides; k >= 1 = a fixed schedule
+    that runs the full network on every k-th step and exits on the others
     (Section 7's schedules; k = 0: exit on every step)."""
     import numpy as np
     import torch
-    e.ee_reset()
-    e.ee_prefill(prompt)
 
     def decode(n):
         if full_every is None:
@@ -86,20 +89,26 @@ def run_condition(e, cfg, tau, exit_layer, prompt, warmup, steps, full_every=Non
         tok, ex, conf, _ = e.ee_decode_n_ex(tau, exit_layer, n, force_exit=sched)
         return tok, ex, conf
 
-    if warmup:
-        decode(warmup)
-    pos0 = e.ee_position()
-    # a one-element kernel that marks the timed launch in profiler traces
-    torch.sigmoid(torch.zeros(1, device="cuda"))
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    tok, ex, conf = decode(steps)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    kernel_ms = e.ee_last_decode_ms()
+    runs = []
+    for _ in range(reps):
+        e.ee_reset()
+        e.ee_prefill(prompt)
+        if warmup:
+            decode(warmup)
+        pos0 = e.ee_position()
+        # a one-element kernel that marks the timed launch in profiler traces
+        torch.sigmoid(torch.zeros(1, device="cuda"))
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        tok, ex, conf = decode(steps)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        runs.append((e.ee_last_decode_ms(), t1 - t0, ex.copy(), pos0))
+    order = sorted(range(reps), key=lambda i: runs[i][0])
+    med = order[reps // 2]
+    kernel_ms, wall, ex, pos0 = runs[med]
     gated = exit_layer > 0
     nbytes = sum(step_bytes(cfg, exit_layer, pos0 + i + 1, bool(ex[i]), gated) for i in range(steps))
-    wall = t1 - t0
     return {
         "tau": None if math.isinf(tau) else float(tau),
         "exit_layer": exit_layer,
@@ -107,10 +116,35 @@ def run_condition(e, cfg, tau, exit_layer, prompt, warmup, steps, full_every=Non
         "tokens_per_s": steps / wall,
         "ms_per_step": 1e3 * wall / steps,
         "kernel_ms": kernel_ms,
+        "kernel_ms_reps": [r[0] for r in runs],
+        "median_rep": med,
         "kernel_tokens_per_s": steps / (kernel_ms * 1e-3),
         "algorithmic_bytes": nbytes,
         "achieved_GBs": nbytes / (kernel_ms * 1e-3) / 1e9,
     }
+
+
+def exit_rate_fit(results, exit_layer, steps):
+    """Least-squares line of the device time per step against the realised
+    exit rate over the conditions at one exit layer, next to the byte model's
+    line (algorithmic bytes per step against the same rates) expressed in
+    time at the bandwidth the fitted intercept implies."""
+    import numpy as np
+    pts = [c for c in results.values() if c.get("exit_layer") == exit_layer and "realised_exit_rate" in c]
+    if len(pts) < 3:
+        return None
+    r = np.array([c["realised_exit_rate"] for c in pts])
+    t = np.array([c["kernel_ms"] / steps for c in pts])
+    b = np.array([c["algorithmic_bytes"] / steps for c in pts])
+    slope, icpt = np.polyfit(r, t, 1)
+    bslope, bicpt = np.polyfit(r, b, 1)
+    model_slope = bslope * icpt / bicpt
+    resid = t - (icpt + slope * r)
+    return {"points": len(pts), "ms_per_step_at_r0": float(icpt), "ms_per_step_per_unit_r": float(slope),
+            "rms_residual_ms": float(np.sqrt(np.mean(resid ** 2))),
+            "byte_model_MB_per_step_at_r0": float(bicpt / 1e6), "byte_model_MB_per_unit_r": float(bslope / 1e6),
+            "byte_model_ms_per_unit_r": float(model_slope),
+            "slope_ratio_measured_to_model": float(slope / model_slope)}
 
 
 def cpu_baseline(cfg, w, prompt, tau, exit_layer, seconds, measure="maxprob"):
@@ -145,6 +179,85 @@ def cpu_baseline(cfg, w, prompt, tau, exit_layer, seconds, measure="maxprob"):
             "sample": (f"fp64 numpy oracle: prefill of the {PROMPT}-token prompt "
                        f"({prefill_s:.1f} s, untimed), then the first {n} gated decode steps "
                        f"at the headline tau (exit rate {exits / n:.2f}) on the host cores")}
+
+
+def measure(e, cfg, w, Le, args):
+    """Calibration, the timed conditions, the refresh and the streaming-read
+    ceiling on one engine."""
+    import torch
+    import synth
+    from paper_2609_14144_amd import EE_CAL_EXIT_RATE
+    e.ee_load_weights(w)
+    e.ee_set_persistent(args.program == "persistent")
+    e.ee_set_confidence_measure(MEASURES[args.confidence])
+    e.ee_set_fill_policy(1 if args.fill == "lazy" else 0)
+    log("weights resident on the GPU")
+
+    cal = [synth.prompts(cfg, 200 + i, PROMPT) for i in range(args.cal_prompts)]
+    rates = [0.5] if args.no_sweep else [0.5, 0.0, 0.96]
+    taus = {}
+    t = time.perf_counter()
+    for r in rates:
+        taus[r] = e.ee_calibrate_threshold(cal, args.cal_gen, Le, EE_CAL_EXIT_RATE, r)
+        log(f"calibrated tau for exit rate {r}: {taus[r]:.4g} ({time.perf_counter() - t:.1f}s)")
+
+    prompt = synth.prompts(cfg, 1, PROMPT)
+    # warm the code path once on another prompt
+    e.ee_reset()
+    e.ee_prefill(synth.prompts(cfg, 2, PROMPT))
+    e.ee_decode_n(taus[0.5], Le, 8)
+
+    results = {}
+    for r in rates:
+        results[f"r{r:g}"] = run_condition(e, cfg, taus[r], Le, prompt, args.warmup, args.steps)
+        log(f"target exit rate {r}: {results[f'r{r:g}']}")
+    if not args.no_sweep:
+        results["ungated"] = run_condition(e, cfg, math.inf, 0, prompt, args.warmup, args.steps)
+        log(f"ungated: {results['ungated']}")
+        # Section 7's fixed schedules, by cost: every step from the readout,
+        # and the full network on every 2nd / 4th step regardless of confidence
+        for name, k in (("always_exit", 0), ("full_every_2nd", 2), ("full_every_4th", 4)):
+            results[name] = run_condition(e, cfg, math.inf, Le, prompt, args.warmup, args.steps, full_every=k)
+            log(f"{name}: {results[name]}")
+    head = results["r0.5"]
+    # periodic full-depth refresh (Section 11) of the 16 most recent positions,
+    # after the last timed run: one launch of 16 full-depth steps
+    rms = []
+    for _ in range(3):
+        e.ee_refresh(16)
+        rms.append(e.ee_last_decode_ms())
+    results["refresh16"] = {"positions": 16, "kernel_ms": sorted(rms)[1],
+                            "full_depth_steps_equivalent": 16}
+    log(f"refresh of 16 positions: {results['refresh16']}")
+
+    # streaming-read ceiling: a plain coalesced 16-byte read of 2 GiB
+    ceiling = e.ee_stream_probe(2 << 30, 5)
+    log(f"streaming-read ceiling: {ceiling:.0f} GB/s")
+
+    kname = "k_decode_persistent" if args.program == "persistent" else "per_op"
+    per_launch = head["algorithmic_bytes"]
+    traffic = None
+    rec = measured_traffic(kname, args.steps, args.warmup, PROMPT)
+    if rec is not None:
+        traffic = rec.get("hbm_bytes_per_launch")
+    roofline = {"bound": "hbm", "achieved": head["achieved_GBs"], "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": head["achieved_GBs"] / PEAK_HBM_GBS, "traffic": traffic,
+                "kernel": kname, "algorithmic_bytes_per_launch": per_launch,
+                "launch_ms": head["kernel_ms"],
+                "ceiling": {"GBs": ceiling, "bytes": 2 << 30,
+                            "probe": "k_stream_read: plain 16-byte coalesced reads of 2 GiB, median of 5"},
+                "frac_of_ceiling": head["achieved_GBs"] / ceiling}
+    prof = os.path.join(ROOT, "profiles", f"{kname}_traffic.json")
+    if os.path.exists(prof):
+        with open(prof) as f:
+            pr = json.load(f)
+        # the committed counter profile, for context when it is not this launch's
+        roofline["traffic_profile"] = {k: pr.get(k) for k in ("steps", "warmup", "prompt", "kernel_source_hash",
+                                                               "ratio_to_algorithmic")}
+    fit = exit_rate_fit(results, Le, args.steps)
+    log(f"time against realised exit rate: {fit}")
+    return results, roofline, taus, fit
+
 
 
 def main():
@@ -199,66 +312,16 @@ def main():
     log(f"weights generated in {time.perf_counter() - t:.1f}s")
     max_seq = PROMPT + max(args.warmup + args.steps, args.cal_gen) + 8
     e = Engine(cfg, max_seq)
-    e.ee_load_weights(w)
-    e.ee_set_persistent(args.program == "persistent")
-    e.ee_set_confidence_measure(MEASURES[args.confidence])
-    e.ee_set_fill_policy(1 if args.fill == "lazy" else 0)
-    log("weights resident on the GPU")
-
-    cal = [synth.prompts(cfg, 200 + i, PROMPT) for i in range(args.cal_prompts)]
-    rates = [0.5] if args.no_sweep else [0.5, 0.0, 0.96]
-    taus = {}
-    t = time.perf_counter()
-    for r in rates:
-        taus[r] = e.ee_calibrate_threshold(cal, args.cal_gen, Le, EE_CAL_EXIT_RATE, r)
-        log(f"calibrated tau for exit rate {r}: {taus[r]:.4g} ({time.perf_counter() - t:.1f}s)")
-
-    prompt = synth.prompts(cfg, 1, PROMPT)
-    # warm the code path once on another prompt
-    e.ee_reset()
-    e.ee_prefill(synth.prompts(cfg, 2, PROMPT))
-    e.ee_decode_n(taus[0.5], Le, 8)
-
-    results = {}
-    for r in rates:
-        results[f"r{r:g}"] = run_condition(e, cfg, taus[r], Le, prompt, args.warmup, args.steps)
-        log(f"target exit rate {r}: {results[f'r{r:g}']}")
-    if not args.no_sweep:
-        results["ungated"] = run_condition(e, cfg, math.inf, 0, prompt, args.warmup, args.steps)
-        log(f"ungated: {results['ungated']}")
-        # Section 7's fixed schedules, by cost: every step from the readout,
-        # and the full network on every 2nd / 4th step regardless of confidence
-        for name, k in (("always_exit", 0), ("full_every_2nd", 2), ("full_every_4th", 4)):
-            results[name] = run_condition(e, cfg, math.inf, Le, prompt, args.warmup, args.steps, full_every=k)
-            log(f"{name}: {results[name]}")
+    try:
+        results, roofline, taus, fit = measure(e, cfg, w, Le, args)
+    finally:
+        # the context is destroyed while the HIP runtime is fully up, not from
+        # a finaliser during interpreter teardown
+        torch.cuda.synchronize()
+        e.close()
+        torch.cuda.synchronize()
     head = results["r0.5"]
-    # periodic full-depth refresh (Section 10) of the 16 most recent positions,
-    # after the last timed run: one launch of 16 full-depth steps
-    rms = []
-    for _ in range(3):
-        e.ee_refresh(16)
-        rms.append(e.ee_last_decode_ms())
-    results["refresh16"] = {"positions": 16, "kernel_ms": sorted(rms)[1],
-                            "full_depth_steps_equivalent": 16}
-    log(f"refresh of 16 positions: {results['refresh16']}")
-
-    # streaming-read ceiling: a plain coalesced 16-byte read of 2 GiB
-    ceiling = e.ee_stream_probe(2 << 30, 5)
-    log(f"streaming-read ceiling: {ceiling:.0f} GB/s")
-
-    kname = "k_decode_persistent" if args.program == "persistent" else "per_op"
-    per_launch = head["algorithmic_bytes"]
-    traffic = None
-    rec = measured_traffic(kname, args.steps)
-    if rec is not None:
-        traffic = rec.get("hbm_bytes_per_launch")
-    roofline = {"bound": "hbm", "achieved": head["achieved_GBs"], "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": head["achieved_GBs"] / PEAK_HBM_GBS, "traffic": traffic,
-                "kernel": kname, "algorithmic_bytes_per_launch": per_launch,
-                "launch_ms": head["kernel_ms"],
-                "ceiling": {"GBs": ceiling, "bytes": 2 << 30,
-                            "probe": "k_stream_read: plain 16-byte coalesced reads of 2 GiB, median of 5"},
-                "frac_of_ceiling": head["achieved_GBs"] / ceiling}
+    prompt = synth.prompts(cfg, 1, PROMPT)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -285,6 +348,7 @@ def main():
                          f"V={cfg.vocab}, {cfg.wdtype}; readout at layer {Le}; {PROMPT}-token prompt, "
                          f"{args.warmup} warm-up + {args.steps} timed decode steps, batch 1; tau "
                          f"calibrated on the GPU to target exit rate 0.5"),
+            "prompt_tokens": PROMPT,
             "exit_layer": Le,
             "target_exit_rate": 0.5,
             "realised_exit_rate": head["realised_exit_rate"],
@@ -296,6 +360,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "sweep": results,
+        "exit_rate_fit": fit,
     }
     print(json.dumps(out), flush=True)
 

@@ -83,7 +83,8 @@ typedef struct ee_config {
   int32_t hidden;     /* H, multiple of 8 */
   int32_t n_q_heads;  /* A */
   int32_t n_kv_heads; /* K, A % K == 0, A/K <= 8 */
-  int32_t head_dim;   /* D, even, D*elem_size a multiple of 16, D <= 256 */
+  int32_t head_dim;   /* D: a KV row of D elements is 128 or 256 bytes
+                         (bf16: D = 64 or 128; fp32: D = 32 or 64) */
   int32_t ffn;        /* F, multiple of 8 */
   int32_t vocab;      /* V */
   float rope_base;    /* rotate-half RoPE base */
@@ -144,7 +145,10 @@ int ee_create(const ee_config* cfg, void* hip_stream, ee_ctx** out);
 int ee_load_weights(ee_ctx* ctx, const ee_tensor* tensors, int32_t n_tensors);
 
 /* Prompt pass at full depth, ungated, over positions pos..pos+n-1 (host token
- * ids in [0,V)). Writes every layer's KV entries and returns in
+ * ids in [0,V)). The gate of Section 4 step five applies to produced tokens;
+ * a prompt runs through the unmodified model, as the prompts of Section 4
+ * step one do, so every layer's cache entries of the prompt are exact.
+ * Writes every layer's KV entries and returns in
  * *out_first_token the full head's argmax at the last prompt position, which
  * becomes the next decode step's input. Synchronous.
  * Errors: EE_ESTATE (weights incomplete), EE_EINVAL (n <= 0, bad token),
@@ -201,7 +205,17 @@ int ee_calibrate_threshold(ee_ctx* ctx, const int32_t* prompts, const int32_t* p
                            int32_t n_prompts, int32_t n_gen, int32_t exit_layer,
                            int32_t mode, float target, float* out_tau);
 
-/* Periodic full-depth refresh (Section 10): recompute the cache entries of
+/* The per-step record of the most recent ee_calibrate_threshold call on ctx
+ * (test hook): confs[i] the readout confidence of recorded step i (prompt by
+ * prompt, n_gen steps each, in order) and, for EE_CAL_NUCLEUS, masses[i] the
+ * full model's probability mass ahead of the readout's token (the token is
+ * acceptable iff it is below 0.9; Section 4 step four); NaN for the other
+ * modes. Host arrays of n entries, either may be NULL.
+ * Errors: EE_ESTATE (no calibration yet), EE_EINVAL (n is not the number of
+ * recorded steps). */
+int ee_calibration_record(ee_ctx* ctx, int32_t n, float* confs, float* masses);
+
+/* Periodic full-depth refresh (Section 11): recompute the cache entries of
  * the n most recent positions at every layer from their own input tokens,
  * replacing the entries projected for exited tokens by the KV-absence fill.
  * Runs the prompt program (full depth, ungated) over those positions, one
@@ -227,7 +241,8 @@ int ee_set_fill_policy(ee_ctx* ctx, int32_t policy);
  * EE_CONF_MAXPROB. Errors: EE_EINVAL (unknown measure). */
 int ee_set_confidence_measure(ee_ctx* ctx, int32_t measure);
 
-/* Replace the offset b (H fp32) of the readout at exit_layer, asynchronously
+/* Replace the offset b (H fp32) of the readout at exit_layer: the offset of
+ * the readout's affine map (Section 4 step two, Appendix B). Asynchronously
  * on the context's stream (no sync): later steps enqueued on the stream see
  * it. Errors: EE_EINVAL (no readout at that layer), EE_EHIP. */
 int ee_set_readout_bias(ee_ctx* ctx, int32_t exit_layer, const float* b, int32_t on_device);

@@ -210,10 +210,11 @@ class OracleDecoder:
         self.pos = t + 1
         return res
 
-    def prefill(self, tokens) -> int:
+    def prefill(self, tokens, progress=None) -> int:
         """Prompt pass at full depth over positions pos..pos+P-1, all layers,
         batched over positions with a causal mask. Returns the first generated
-        token (argmax of the full head at the last prompt position)."""
+        token (argmax of the full head at the last prompt position).
+        progress, if given, is called with each layer index once it is done."""
         c = self.cfg
         tokens = np.asarray(tokens, dtype=np.int64)
         P = tokens.size
@@ -247,6 +248,8 @@ class OracleDecoder:
             H = H + o.reshape(P, -1) @ lw["wo"].T
             m = rmsnorm(H, lw["g_mlp"], c.rms_eps)
             H = H + (silu(m @ lw["wg"].T) * (m @ lw["wu"].T)) @ lw["wd"].T
+            if progress is not None:
+                progress(l)
         self.pos = T
         self.last_prefill_stats = head_stats(self.full_logits(H[-1]))  # (token, conf, gap)
         return self.last_prefill_stats[0]
@@ -255,7 +258,7 @@ class OracleDecoder:
         """Full-depth pass over the n most recent positions with their own
         input tokens: their cache entries at every layer are recomputed
         exactly, replacing the entries the KV-absence fill projected for
-        exited tokens (Section 10: a periodic full-depth pass over the most
+        exited tokens (Section 11: a periodic full-depth pass over the most
         recent tokens recovers the drift of the reconstructed cache). The
         position and the next input are unchanged."""
         if not (1 <= n <= self.pos):

@@ -73,6 +73,7 @@ def _load():
         "ee_decode_step_ex": (C.c_int, [V, C.c_float, C.c_int32, C.c_int32, C.c_int32, C.POINTER(ee_debug)]),
         "ee_calibrate_threshold": (C.c_int, [V, _IP, _IP, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                              C.c_float, _FP]),
+        "ee_calibration_record": (C.c_int, [V, C.c_int32, _FP, _FP]),
         "ee_set_readout_bias": (C.c_int, [V, C.c_int32, _FP, C.c_int32]),
         "ee_set_confidence_measure": (C.c_int, [V, C.c_int32]),
         "ee_refresh": (C.c_int, [V, C.c_int32]),
@@ -216,6 +217,13 @@ class Engine:
                                                len(prompts), n_gen, exit_layer, mode, target,
                                                C.byref(tau)))
         return tau.value
+
+    def ee_calibration_record(self, n: int):
+        """(confidences, masses) of the latest calibration's n recorded steps."""
+        confs = np.empty(n, np.float32)
+        masses = np.empty(n, np.float32)
+        self._check(lib.ee_calibration_record(self._ctx, int(n), _ptr(confs, C.c_float), _ptr(masses, C.c_float)))
+        return confs, masses
 
     def ee_set_readout_bias(self, exit_layer: int, b):
         b = np.ascontiguousarray(b, dtype=np.float32)

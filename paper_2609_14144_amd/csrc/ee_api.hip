@@ -10,6 +10,7 @@
 #include <new>
 #include <random>
 #include <set>
+#include <stdexcept>
 #include <string>
 #include <vector>
 
@@ -66,6 +67,7 @@ struct ee_ctx {
   int32_t *d_ring_tok = nullptr, *d_ring_exit = nullptr, *d_ring_would = nullptr;
   float* d_ring_conf = nullptr;
   float* d_ring_mass = nullptr;
+  std::vector<float> cal_confs, cal_masses;  // record of the latest calibration (test hook)
   bool fill_lazy = false;  // persistent program: batch the KV fill of consecutive exits
   int fill_slots = 0;      // exit-layer states one batched fill can take
   bool nucleus = false;   // steps also measure the readout token's nucleus rank (calibration, debug)
@@ -117,6 +119,34 @@ void give_slot(int i) {
 int fail(ee_ctx* c, int code, const std::string& msg) {
   if (c) c->err = msg;
   return code;
+}
+
+// Record a message for an exception caught at the ABI (never throws: a
+// failed assignment leaves the message empty).
+void note_exception(ee_ctx* c, const char* msg) noexcept {
+  try {
+    if (c) c->err = msg;
+    else g_create_err = msg;
+  } catch (...) {
+    if (c) c->err.clear();
+    else g_create_err.clear();
+  }
+}
+
+template <typename F>
+int guarded(ee_ctx* c, F&& f) noexcept {
+  try {
+    return f();
+  } catch (const std::bad_alloc&) {
+    note_exception(c, "out of host memory");
+    return EE_ENOMEM;
+  } catch (const std::length_error&) {
+    note_exception(c, "out of host memory (size limit)");
+    return EE_ENOMEM;
+  } catch (...) {
+    note_exception(c, "unexpected C++ exception inside the library");
+    return EE_EINVAL;
+  }
 }
 
 int hip_fail(ee_ctx* c, hipError_t e, const char* what) {
@@ -177,6 +207,28 @@ int validate_config(const ee_config* g, std::string& why) {
   if (!is_pow2(g->page_size)) { why = "page_size must be a power of two"; return 0; }
   if (!(g->rms_eps > 0.f) || !(g->rope_base > 0.f)) { why = "rms_eps and rope_base must be positive"; return 0; }
   return 1;
+}
+
+// The tagged activation words of a decode call, in one block: h, h_exit
+// (kMaxPending slots), z, q, o, a, this step's K/V row, the gate record and
+// the attention partial records, each part starting on a 256-byte boundary.
+constexpr int kTwParts = 9;
+int64_t tw_layout(const ee_config& g, int64_t off[kTwParts]) {
+  const int64_t H = g.hidden, A = g.n_q_heads, K = g.n_kv_heads, D = g.head_dim, F = g.ffn;
+  const int64_t pairs = ((A / K) + 1) / 2;
+  const int64_t splits = (g.max_seq + ee::kAttnSplit - 1) / ee::kAttnSplit;
+  const int64_t sizes[kTwParts] = {H, int64_t(ee::kMaxPending) * H, H, A * D, A * D, F, 2 * K * D, 8,
+                                   K * pairs * splits * (2 * D + 4)};
+  int64_t total = 0;
+  for (int i = 0; i < kTwParts; ++i) {
+    off[i] = total;
+    total += (sizes[i] + 31) & ~int64_t(31);
+  }
+  return total;
+}
+
+void tw_bind(uint64_t* base, const int64_t off[kTwParts], uint64_t** const ptrs[kTwParts]) {
+  for (int i = 0; i < kTwParts; ++i) *ptrs[i] = base + off[i];
 }
 
 DevParams make_params(const ee_ctx* c, float tau, int exit_layer) {
@@ -499,7 +551,9 @@ int load_one(ee_ctx* c, const ee_tensor& t) {
 
 extern "C" {
 
-int ee_create(const ee_config* cfg, void* hip_stream, ee_ctx** out) {
+static int create_body(ee_ctx* c, const ee_config* cfg, void* hip_stream, ee_ctx** out);
+
+static int create_impl(const ee_config* cfg, void* hip_stream, ee_ctx** out) {
   if (!cfg || !out) return EE_EINVAL;
   *out = nullptr;
   std::string why;
@@ -513,6 +567,15 @@ int ee_create(const ee_config* cfg, void* hip_stream, ee_ctx** out) {
     g_create_err = "out of host memory";
     return EE_ENOMEM;
   }
+  try {
+    return create_body(c, cfg, hip_stream, out);
+  } catch (...) {
+    ee_destroy(c);
+    throw;
+  }
+}
+
+static int create_body(ee_ctx* c, const ee_config* cfg, void* hip_stream, ee_ctx** out) {
   c->cfg = *cfg;
   c->wbf16 = cfg->wdtype == EE_BF16;
   c->esz = c->wbf16 ? 2 : 4;
@@ -586,22 +649,13 @@ int ee_create(const ee_config* cfg, void* hip_stream, ee_ctx** out) {
   }
   c->max_splits = (g.max_seq + ee::kAttnSplit - 1) / ee::kAttnSplit;
   {
-    const int64_t pairs = ((A / K) + 1) / 2;
-    const int64_t sizes[9] = {int64_t(H), int64_t(ee::kMaxPending) * int64_t(H), int64_t(H), int64_t(A * D),
-                              int64_t(A * D),
-                              int64_t(F), int64_t(2 * K * D), 8,
-                              int64_t(K) * pairs * c->max_splits * int64_t(2 * D + 4)};
-    uint64_t** ptrs[9] = {&c->d_h, &c->d_hexit, &c->d_z, &c->d_q, &c->d_o, &c->d_a, &c->d_kvnew, &c->d_dec,
-                          &c->d_attn_part};
-    int64_t total = 0;
-    for (int i = 0; i < 9; ++i) total += (sizes[i] + 31) & ~int64_t(31);  // 256-byte aligned parts
+    int64_t off[kTwParts];
+    const int64_t total = tw_layout(g, off);
+    uint64_t** const ptrs[kTwParts] = {&c->d_h, &c->d_hexit, &c->d_z, &c->d_q, &c->d_o, &c->d_a,
+                                       &c->d_kvnew, &c->d_dec, &c->d_attn_part};
     if ((r = dalloc(c, &c->d_tw, total * 8)) || (r = dalloc(c, &c->d_x, H * 4))) return bail(r);
     c->tw_words = total;
-    int64_t off = 0;
-    for (int i = 0; i < 9; ++i) {
-      *ptrs[i] = c->d_tw + off;
-      off += (sizes[i] + 31) & ~int64_t(31);
-    }
+    tw_bind(c->d_tw, off, ptrs);
     if ((he = hipMemset(c->d_tw, 0, total * 8)) != hipSuccess) return bail(hip_fail(c, he, "hipMemset"));
   }
   if ((r = dalloc(c, &c->d_hist, sizeof(int32_t) * g.max_seq))) return bail(r);
@@ -634,7 +688,7 @@ int ee_create(const ee_config* cfg, void* hip_stream, ee_ctx** out) {
   return EE_OK;
 }
 
-int ee_load_weights(ee_ctx* c, const ee_tensor* tensors, int32_t n_tensors) {
+static int load_weights_impl(ee_ctx* c, const ee_tensor* tensors, int32_t n_tensors) {
   if (!c) return EE_EINVAL;
   c->err.clear();
   if (!tensors || n_tensors < 0) return fail(c, EE_EINVAL, "bad tensor list");
@@ -647,7 +701,7 @@ int ee_load_weights(ee_ctx* c, const ee_tensor* tensors, int32_t n_tensors) {
   return EE_OK;
 }
 
-int ee_prefill(ee_ctx* c, const int32_t* tokens, int32_t n, int32_t* out_first_token) {
+static int prefill_impl(ee_ctx* c, const int32_t* tokens, int32_t n, int32_t* out_first_token) {
   if (!c) return EE_EINVAL;
   c->err.clear();
   if (!weights_ready(c)) return fail(c, EE_ESTATE, "weights not fully loaded");
@@ -661,7 +715,7 @@ int ee_prefill(ee_ctx* c, const int32_t* tokens, int32_t n, int32_t* out_first_t
   return EE_OK;
 }
 
-int ee_refresh(ee_ctx* c, int32_t n) {
+static int refresh_impl(ee_ctx* c, int32_t n) {
   if (!c) return EE_EINVAL;
   c->err.clear();
   if (!weights_ready(c)) return fail(c, EE_ESTATE, "weights not fully loaded");
@@ -686,7 +740,7 @@ int ee_refresh(ee_ctx* c, int32_t n) {
   return EE_OK;
 }
 
-int ee_decode_n_ex(ee_ctx* c, float tau, int32_t exit_layer, int32_t n, const int32_t* force_tokens,
+static int decode_n_ex_impl(ee_ctx* c, float tau, int32_t exit_layer, int32_t n, const int32_t* force_tokens,
                    const int32_t* force_exit, int32_t* tokens, int32_t* exited, float* conf,
                    int32_t* would_exit) {
   int r = decode_common(c, tau, exit_layer, n, force_tokens, force_exit, false);
@@ -694,18 +748,18 @@ int ee_decode_n_ex(ee_ctx* c, float tau, int32_t exit_layer, int32_t n, const in
   return copy_ring(c, n, tokens, exited, conf, would_exit);
 }
 
-int ee_decode_n(ee_ctx* c, float tau, int32_t exit_layer, int32_t n, int32_t* tokens,
+static int decode_n_impl(ee_ctx* c, float tau, int32_t exit_layer, int32_t n, int32_t* tokens,
                 int32_t* exited, float* conf) {
   return ee_decode_n_ex(c, tau, exit_layer, n, nullptr, nullptr, tokens, exited, conf, nullptr);
 }
 
-int ee_decode_step(ee_ctx* c, float tau, int32_t exit_layer, int32_t* out_token,
+static int decode_step_impl(ee_ctx* c, float tau, int32_t exit_layer, int32_t* out_token,
                    int32_t* out_exited, float* out_conf) {
   return ee_decode_n_ex(c, tau, exit_layer, 1, nullptr, nullptr, out_token, out_exited, out_conf,
                         nullptr);
 }
 
-int ee_decode_step_ex(ee_ctx* c, float tau, int32_t exit_layer, int32_t input_token,
+static int decode_step_ex_impl(ee_ctx* c, float tau, int32_t exit_layer, int32_t input_token,
                       int32_t force_exit, ee_debug* dbg) {
   if (!c) return EE_EINVAL;
   c->err.clear();
@@ -748,7 +802,7 @@ int ee_decode_step_ex(ee_ctx* c, float tau, int32_t exit_layer, int32_t input_to
   return EE_OK;
 }
 
-int ee_calibrate_threshold(ee_ctx* c, const int32_t* prompts, const int32_t* prompt_lens,
+static int calibrate_threshold_impl(ee_ctx* c, const int32_t* prompts, const int32_t* prompt_lens,
                            int32_t n_prompts, int32_t n_gen, int32_t exit_layer, int32_t mode,
                            float target, float* out_tau) {
   if (!c) return EE_EINVAL;
@@ -782,6 +836,9 @@ int ee_calibrate_threshold(ee_ctx* c, const int32_t* prompts, const int32_t* pro
     off += prompt_lens[i];
   }
   if ((r = ee_reset(c))) return r;
+  c->cal_confs = confs;
+  c->cal_masses = masses;
+  if (mode != EE_CAL_NUCLEUS) c->cal_masses.assign(confs.size(), NAN);
   if (mode == EE_CAL_NUCLEUS) {
     // the lowest grid threshold whose early answers are acceptable often enough
     *out_tau = INFINITY;
@@ -816,7 +873,18 @@ int ee_calibrate_threshold(ee_ctx* c, const int32_t* prompts, const int32_t* pro
   return EE_OK;
 }
 
-int ee_set_readout_bias(ee_ctx* c, int32_t exit_layer, const float* b, int32_t on_device) {
+static int calibration_record_impl(ee_ctx* c, int32_t n, float* confs, float* masses) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  if (c->cal_confs.empty()) return fail(c, EE_ESTATE, "no calibration has run on this context");
+  if (n != static_cast<int32_t>(c->cal_confs.size()))
+    return fail(c, EE_EINVAL, "the latest calibration recorded " + std::to_string(c->cal_confs.size()) + " steps");
+  if (confs) memcpy(confs, c->cal_confs.data(), sizeof(float) * n);
+  if (masses) memcpy(masses, c->cal_masses.data(), sizeof(float) * n);
+  return EE_OK;
+}
+
+static int set_readout_bias_impl(ee_ctx* c, int32_t exit_layer, const float* b, int32_t on_device) {
   if (!c) return EE_EINVAL;
   c->err.clear();
   auto it = c->readout.find(exit_layer);
@@ -826,7 +894,7 @@ int ee_set_readout_bias(ee_ctx* c, int32_t exit_layer, const float* b, int32_t o
   return EE_OK;
 }
 
-int ee_set_fill_policy(ee_ctx* c, int32_t policy) {
+static int set_fill_policy_impl(ee_ctx* c, int32_t policy) {
   if (!c) return EE_EINVAL;
   c->err.clear();
   if (policy != EE_FILL_EAGER && policy != EE_FILL_LAZY) return fail(c, EE_EINVAL, "unknown fill policy");
@@ -834,7 +902,7 @@ int ee_set_fill_policy(ee_ctx* c, int32_t policy) {
   return EE_OK;
 }
 
-int ee_stream_probe(ee_ctx* c, int64_t bytes, int32_t reps, float* out_gbps) {
+static int stream_probe_impl(ee_ctx* c, int64_t bytes, int32_t reps, float* out_gbps) {
   if (!c) return EE_EINVAL;
   c->err.clear();
   if (!out_gbps || bytes < 16 || reps < 1) return fail(c, EE_EINVAL, "stream probe: bytes >= 16, reps >= 1, output");
@@ -867,7 +935,7 @@ int ee_stream_probe(ee_ctx* c, int64_t bytes, int32_t reps, float* out_gbps) {
   return EE_OK;
 }
 
-int ee_set_confidence_measure(ee_ctx* c, int32_t measure) {
+static int set_confidence_measure_impl(ee_ctx* c, int32_t measure) {
   if (!c) return EE_EINVAL;
   c->err.clear();
   if (measure != EE_CONF_MAXPROB && measure != EE_CONF_MARGIN && measure != EE_CONF_NEGENTROPY)
@@ -876,7 +944,7 @@ int ee_set_confidence_measure(ee_ctx* c, int32_t measure) {
   return EE_OK;
 }
 
-int ee_head_eval(ee_ctx* c, int32_t readout_layer, const float* x, int32_t* out_token,
+static int head_eval_impl(ee_ctx* c, int32_t readout_layer, const float* x, int32_t* out_token,
                  float* out_conf, float* out_logits) {
   if (!c) return EE_EINVAL;
   c->err.clear();
@@ -912,7 +980,7 @@ int ee_head_eval(ee_ctx* c, int32_t readout_layer, const float* x, int32_t* out_
   return EE_OK;
 }
 
-int ee_read_kv(ee_ctx* c, int32_t layer, int32_t pos, float* k_out, float* v_out) {
+static int read_kv_impl(ee_ctx* c, int32_t layer, int32_t pos, float* k_out, float* v_out) {
   if (!c) return EE_EINVAL;
   c->err.clear();
   if (layer < 0 || layer >= c->cfg.n_layers || pos < 0 || pos >= c->pos)
@@ -949,7 +1017,7 @@ int ee_read_kv(ee_ctx* c, int32_t layer, int32_t pos, float* k_out, float* v_out
   return EE_OK;
 }
 
-int ee_set_persistent(ee_ctx* c, int32_t wgs_per_cu) {
+static int set_persistent_impl(ee_ctx* c, int32_t wgs_per_cu) {
   if (!c) return EE_EINVAL;
   c->err.clear();
   if (wgs_per_cu == 0) {
@@ -966,7 +1034,7 @@ int ee_set_persistent(ee_ctx* c, int32_t wgs_per_cu) {
   return EE_OK;
 }
 
-int ee_set_persistent_grid(ee_ctx* c, int32_t nwg) {
+static int set_persistent_grid_impl(ee_ctx* c, int32_t nwg) {
   if (!c) return EE_EINVAL;
   c->err.clear();
   const int most = std::min(c->max_parts, c->n_cu * c->max_wgs_per_cu);
@@ -978,7 +1046,7 @@ int ee_set_persistent_grid(ee_ctx* c, int32_t nwg) {
   return EE_OK;
 }
 
-int ee_set_timeline(ee_ctx* c, int32_t capacity) {
+static int set_timeline_impl(ee_ctx* c, int32_t capacity) {
   if (!c) return EE_EINVAL;
   c->err.clear();
   if (capacity < 0) return fail(c, EE_EINVAL, "capacity must be >= 0");
@@ -994,7 +1062,7 @@ int ee_set_timeline(ee_ctx* c, int32_t capacity) {
   return EE_OK;
 }
 
-int ee_read_timeline(ee_ctx* c, uint64_t* out, int32_t n) {
+static int read_timeline_impl(ee_ctx* c, uint64_t* out, int32_t n) {
   if (!c || !out || n < 0) return EE_EINVAL;
   c->err.clear();
   if (n > c->timeline_cap) return fail(c, EE_EINVAL, "more entries requested than recorded");
@@ -1003,7 +1071,7 @@ int ee_read_timeline(ee_ctx* c, uint64_t* out, int32_t n) {
   return EE_OK;
 }
 
-int ee_last_decode_ms(ee_ctx* c, float* out_ms) {
+static int last_decode_ms_impl(ee_ctx* c, float* out_ms) {
   if (!c || !out_ms) return EE_EINVAL;
   *out_ms = c->last_ms;
   return EE_OK;
@@ -1011,7 +1079,7 @@ int ee_last_decode_ms(ee_ctx* c, float* out_ms) {
 
 int32_t ee_position(const ee_ctx* c) { return c ? c->pos : -1; }
 
-int ee_reset(ee_ctx* c) {
+static int reset_impl(ee_ctx* c) {
   if (!c) return EE_EINVAL;
   c->err.clear();
   HIPCHK(c, hipStreamSynchronize(c->stream));
@@ -1026,7 +1094,7 @@ int ee_reset(ee_ctx* c) {
 
 const char* ee_last_error(const ee_ctx* c) { return c ? c->err.c_str() : g_create_err.c_str(); }
 
-void ee_destroy(ee_ctx* c) {
+static void destroy_impl(ee_ctx* c) {
   if (!c) return;
   if (c->stream) (void)hipStreamSynchronize(c->stream);
   dfree(c->embed);
@@ -1055,6 +1123,90 @@ void ee_destroy(ee_ctx* c) {
   if (c->params_pinned) (void)hipHostFree(c->params_pinned);
   give_slot(c->slot);
   delete c;
+}
+
+
+// Every entry point runs its body under guarded(): no C++ exception
+// (std::bad_alloc from a container, for instance) crosses the C ABI.
+int ee_create(const ee_config* cfg, void* hip_stream, ee_ctx** out) {
+  return guarded(nullptr, [&]() { return create_impl(cfg, hip_stream, out); });
+}
+int ee_load_weights(ee_ctx* c, const ee_tensor* tensors, int32_t n_tensors) {
+  return guarded(c, [&]() { return load_weights_impl(c, tensors, n_tensors); });
+}
+int ee_prefill(ee_ctx* c, const int32_t* tokens, int32_t n, int32_t* out_first_token) {
+  return guarded(c, [&]() { return prefill_impl(c, tokens, n, out_first_token); });
+}
+int ee_refresh(ee_ctx* c, int32_t n) {
+  return guarded(c, [&]() { return refresh_impl(c, n); });
+}
+int ee_decode_n_ex(ee_ctx* c, float tau, int32_t exit_layer, int32_t n, const int32_t* force_tokens,
+                   const int32_t* force_exit, int32_t* tokens, int32_t* exited, float* conf,
+                   int32_t* would_exit) {
+  return guarded(c, [&]() { return decode_n_ex_impl(c, tau, exit_layer, n, force_tokens, force_exit, tokens, exited, conf, would_exit); });
+}
+int ee_decode_n(ee_ctx* c, float tau, int32_t exit_layer, int32_t n, int32_t* tokens,
+                int32_t* exited, float* conf) {
+  return guarded(c, [&]() { return decode_n_impl(c, tau, exit_layer, n, tokens, exited, conf); });
+}
+int ee_decode_step(ee_ctx* c, float tau, int32_t exit_layer, int32_t* out_token,
+                   int32_t* out_exited, float* out_conf) {
+  return guarded(c, [&]() { return decode_step_impl(c, tau, exit_layer, out_token, out_exited, out_conf); });
+}
+int ee_decode_step_ex(ee_ctx* c, float tau, int32_t exit_layer, int32_t input_token,
+                      int32_t force_exit, ee_debug* dbg) {
+  return guarded(c, [&]() { return decode_step_ex_impl(c, tau, exit_layer, input_token, force_exit, dbg); });
+}
+int ee_calibrate_threshold(ee_ctx* c, const int32_t* prompts, const int32_t* prompt_lens,
+                           int32_t n_prompts, int32_t n_gen, int32_t exit_layer, int32_t mode,
+                           float target, float* out_tau) {
+  return guarded(c, [&]() { return calibrate_threshold_impl(c, prompts, prompt_lens, n_prompts, n_gen, exit_layer, mode, target, out_tau); });
+}
+int ee_calibration_record(ee_ctx* c, int32_t n, float* confs, float* masses) {
+  return guarded(c, [&]() { return calibration_record_impl(c, n, confs, masses); });
+}
+int ee_set_readout_bias(ee_ctx* c, int32_t exit_layer, const float* b, int32_t on_device) {
+  return guarded(c, [&]() { return set_readout_bias_impl(c, exit_layer, b, on_device); });
+}
+int ee_set_fill_policy(ee_ctx* c, int32_t policy) {
+  return guarded(c, [&]() { return set_fill_policy_impl(c, policy); });
+}
+int ee_stream_probe(ee_ctx* c, int64_t bytes, int32_t reps, float* out_gbps) {
+  return guarded(c, [&]() { return stream_probe_impl(c, bytes, reps, out_gbps); });
+}
+int ee_set_confidence_measure(ee_ctx* c, int32_t measure) {
+  return guarded(c, [&]() { return set_confidence_measure_impl(c, measure); });
+}
+int ee_head_eval(ee_ctx* c, int32_t readout_layer, const float* x, int32_t* out_token,
+                 float* out_conf, float* out_logits) {
+  return guarded(c, [&]() { return head_eval_impl(c, readout_layer, x, out_token, out_conf, out_logits); });
+}
+int ee_read_kv(ee_ctx* c, int32_t layer, int32_t pos, float* k_out, float* v_out) {
+  return guarded(c, [&]() { return read_kv_impl(c, layer, pos, k_out, v_out); });
+}
+int ee_set_persistent(ee_ctx* c, int32_t wgs_per_cu) {
+  return guarded(c, [&]() { return set_persistent_impl(c, wgs_per_cu); });
+}
+int ee_set_persistent_grid(ee_ctx* c, int32_t nwg) {
+  return guarded(c, [&]() { return set_persistent_grid_impl(c, nwg); });
+}
+int ee_set_timeline(ee_ctx* c, int32_t capacity) {
+  return guarded(c, [&]() { return set_timeline_impl(c, capacity); });
+}
+int ee_read_timeline(ee_ctx* c, uint64_t* out, int32_t n) {
+  return guarded(c, [&]() { return read_timeline_impl(c, out, n); });
+}
+int ee_last_decode_ms(ee_ctx* c, float* out_ms) {
+  return guarded(c, [&]() { return last_decode_ms_impl(c, out_ms); });
+}
+int ee_reset(ee_ctx* c) {
+  return guarded(c, [&]() { return reset_impl(c); });
+}
+void ee_destroy(ee_ctx* c) {
+  try {
+    destroy_impl(c);
+  } catch (...) {
+  }
 }
 
 }  // extern "C"

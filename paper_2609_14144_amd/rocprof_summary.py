@@ -54,9 +54,12 @@ def _bench_json(path):
 
 
 def _timed(dispatches, bench):
-    """The decode dispatches of the timed launches: for each condition of the
-    sweep, in order, the first decode dispatch after bench.py's marker."""
-    conds = [(k, c) for k, c in bench["sweep"].items() if "realised_exit_rate" in c]
+    """The decode dispatches of the timed launches: every condition of the
+    sweep is timed `len(kernel_ms_reps)` times, in order, and each timed
+    launch is the first decode dispatch after bench.py's marker kernel.
+    Returns [((name, condition, rep), dispatch)]."""
+    conds = [(k, c, i) for k, c in bench["sweep"].items() if "realised_exit_rate" in c
+             for i in range(len(c.get("kernel_ms_reps", [c["kernel_ms"]])))]
     rows = sorted(dispatches, key=lambda d: int(d["Dispatch_Id"]))
     out = []
     marks = [i for i, d in enumerate(rows) if MARKER_KERNEL in d["Kernel_Name"]]
@@ -65,8 +68,12 @@ def _timed(dispatches, bench):
         if nxt is not None:
             out.append(nxt)
     if len(out) != len(conds):
-        sys.exit(f"found {len(out)} marked decode launches for {len(conds)} conditions")
+        sys.exit(f"found {len(out)} marked decode launches for {len(conds)} timed launches")
     return list(zip(conds, out))
+
+
+def _rep_ms(c, rep):
+    return c.get("kernel_ms_reps", [c["kernel_ms"]])[rep]
 
 
 def trace(args):
@@ -87,12 +94,14 @@ def trace(args):
                    f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
                    f"{float(r['MaxNs']) / 1e3:.2f} |")
     out += ["", "## Timed decode launches (one persistent launch of `steps` decode steps each)", "",
-            "| condition | exit rate | steps | rocprof duration ms | bench HIP-event ms | difference |",
-            "|---|---|---|---|---|---|"]
-    for (name, c), d in _timed(disp, bench):
+            "| condition | repetition | exit rate | steps | rocprof duration ms | bench HIP-event ms | difference |",
+            "|---|---|---|---|---|---|---|"]
+    for (name, c, rep), d in _timed(disp, bench):
         dur = (int(d["End_Timestamp"]) - int(d["Start_Timestamp"])) / 1e6
-        out.append(f"| {name} | {c['realised_exit_rate']:.3f} | {bench['steps']} | {dur:.3f} | "
-                   f"{c['kernel_ms']:.3f} | {100 * (dur / c['kernel_ms'] - 1):+.2f}% |")
+        ms = _rep_ms(c, rep)
+        med = " (median)" if rep == c.get("median_rep", 0) else ""
+        out.append(f"| {name} | {rep}{med} | {c['realised_exit_rate']:.3f} | {bench['steps']} | {dur:.3f} | "
+                   f"{ms:.3f} | {100 * (dur / ms - 1):+.2f}% |")
     rf = bench["roofline"]
     out += ["", f"Headline (bench JSON): {bench['value']:.1f} {bench['unit']}; roofline achieved "
             f"{rf['achieved']:.1f} GB/s of {rf['peak']:.0f} GB/s (frac {rf['frac']:.4f}) from "
@@ -119,7 +128,8 @@ def _counter(d, name):
 def traffic(args):
     bench = _bench_json(args.bench)
     rec = {"kernel": KERNEL, "kernel_source_hash": kernel_source_hash(),
-           "workload": bench["config"]["workload"], "steps": bench["steps"],
+           "workload": bench["config"]["workload"], "steps": bench["steps"], "warmup": bench["warmup"],
+           "prompt": bench["config"].get("prompt_tokens"),
            "command_fetch": args.command_fetch, "command_write": args.command_write,
            "copy_probe_mib": args.copy_mib}
     total = 0.0
@@ -130,7 +140,9 @@ def traffic(args):
             sys.exit(f"{key}: no copy-probe dispatch")
         expect_kib = args.copy_mib * 1024.0
         scale = float(copy[0]["Counter_Value"]) / expect_kib  # counter units per KiB moved
-        (name, _), headline = _timed(rows, bench)[0]
+        timed = _timed(rows, bench)
+        (name, c, _), headline = next(((k, d) for k, d in timed if k[0] == "r0.5" and
+                                       k[2] == bench["sweep"]["r0.5"].get("median_rep", 0)))
         b = float(headline["Counter_Value"]) / scale * 1024.0
         rec[key.lower()] = {"copy_counter_kib": float(copy[0]["Counter_Value"]), "copy_expected_kib": expect_kib,
                             "scale": scale, "raw_kib": float(headline["Counter_Value"]), "bytes": b,

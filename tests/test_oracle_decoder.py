@@ -269,7 +269,7 @@ def test_tau_nucleus_grid():
 
 
 def test_refresh_restores_the_full_depth_cache(w):
-    """A full-depth pass over every decoded position (Section 10's periodic
+    """A full-depth pass over every decoded position (Section 11's periodic
     refresh) replaces the projected entries of exited tokens with the cache
     an ungated run over the same tokens writes; the next step then matches
     the ungated model's."""
