@@ -171,6 +171,24 @@ int ee_decode_step(ee_ctx* ctx, float tau, int32_t exit_layer,
 int ee_decode_n(ee_ctx* ctx, float tau, int32_t exit_layer, int32_t n,
                 int32_t* tokens, int32_t* exited, float* conf);
 
+/* ee_decode_n for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * it calls no hipMalloc, hipFree or other allocating routine. The outputs
+ * go to caller-owned device arrays of n entries on the context's device
+ * (d_tokens, d_exited as 0/1, d_conf; none may be NULL), and the call's
+ * working set (tagged activation words, attention and head partial records,
+ * barrier counters) lives in a library-resident scratch array of 4 MiB per
+ * device, held until the process ends, instead of the context's own
+ * buffers. The scratch is cleared at the start of every call. All calls on
+ * one device share that device's scratch: calls that overlap in time on one
+ * device (several contexts on different streams) race, and the caller must
+ * order them. One sync at the end, as ee_decode_n; the results equal
+ * ee_decode_n's. Errors as ee_decode_n, plus EE_EINVAL for a NULL output
+ * and EE_ECAPACITY when the context's working set (it grows with max_seq
+ * through the attention partial records) exceeds the scratch. */
+int ee_decode_n_noalloc(ee_ctx* ctx, float tau, int32_t exit_layer, int32_t n,
+                        int32_t* d_tokens, int32_t* d_exited, float* d_conf);
+
 /* ee_decode_n with optional imposed inputs (host arrays of n, may be NULL):
  * force_tokens[i] replaces step i's input token (teacher forcing; the first
  * step may then run without a prior prefill output), force_exit[i] is -1

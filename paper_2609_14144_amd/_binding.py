@@ -70,6 +70,7 @@ def _load():
         "ee_decode_step": (C.c_int, [V, C.c_float, C.c_int32, _IP, _IP, _FP]),
         "ee_decode_n": (C.c_int, [V, C.c_float, C.c_int32, C.c_int32, _IP, _IP, _FP]),
         "ee_decode_n_ex": (C.c_int, [V, C.c_float, C.c_int32, C.c_int32, _IP, _IP, _IP, _IP, _FP, _IP]),
+        "ee_decode_n_noalloc": (C.c_int, [V, C.c_float, C.c_int32, C.c_int32, V, V, V]),
         "ee_decode_step_ex": (C.c_int, [V, C.c_float, C.c_int32, C.c_int32, C.c_int32, C.POINTER(ee_debug)]),
         "ee_calibrate_threshold": (C.c_int, [V, _IP, _IP, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                              C.c_float, _FP]),
@@ -188,6 +189,14 @@ class Engine:
                                        _ptr(fe, C.c_int32), _ptr(tok, C.c_int32), _ptr(ex, C.c_int32),
                                        _ptr(conf, C.c_float), _ptr(would, C.c_int32)))
         return tok, ex.astype(bool), conf, would.astype(bool)
+
+    def ee_decode_n_noalloc(self, tau: float, exit_layer: int, n: int, d_tokens: int, d_exited: int,
+                            d_conf: int):
+        """Outputs go to caller-owned device arrays (raw device addresses, for
+        instance torch tensors' data_ptr()): n int32 tokens, n int32 exit
+        flags, n float32 confidences."""
+        self._check(lib.ee_decode_n_noalloc(self._ctx, tau, exit_layer, n, C.c_void_p(d_tokens),
+                                            C.c_void_p(d_exited), C.c_void_p(d_conf)))
 
     def ee_decode_step_ex(self, tau: float, exit_layer: int, input_token: int = -1,
                           force_exit: int = -1, debug: bool = True) -> dict:

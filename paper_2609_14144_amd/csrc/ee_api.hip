@@ -90,6 +90,7 @@ struct ee_ctx {
   uint64_t* d_timeline = nullptr;
   int timeline_cap = 0;
   DevParams* params_pinned = nullptr;  // staging of the parameter block
+  void* scratch = nullptr;             // this device's library-resident scratch (ee_decode_n_noalloc)
   std::string err;
 };
 
@@ -338,16 +339,61 @@ int check_gate_args(ee_ctx* c, float tau, int exit_layer) {
   return EE_OK;
 }
 
-// Launch n steps (decode, or prompt positions when prefill) and wait.
+// Caller-owned device outputs of an allocation-free decode call; its working
+// set is bound to the library-resident scratch.
+struct NoAlloc {
+  int32_t* tok;
+  int32_t* exited;
+  float* conf;
+};
+
+// Bytes of the scratch a decode call of this context uses: the tagged words,
+// the head partial records and the barrier counters.
+size_t scratch_need(const ee_ctx* c, int64_t off[kTwParts], size_t* head_off, size_t* ctr_off) {
+  const int64_t words = tw_layout(c->cfg, off);
+  size_t b = static_cast<size_t>(words) * 8;
+  *head_off = b;
+  b += (static_cast<size_t>(c->max_parts) * ee::kStatFloats * 4 + 255) & ~size_t(255);
+  *ctr_off = b;
+  return b + ((sizeof(ee::Counters) + 255) & ~size_t(255));
+}
+
+int bind_scratch(ee_ctx* c, DevParams& p) {
+  int64_t off[kTwParts];
+  size_t head_off, ctr_off;
+  const size_t need = scratch_need(c, off, &head_off, &ctr_off);
+  if (need > ee::kScratchBytes)
+    return fail(c, EE_ECAPACITY, "this context's decode working set needs " + std::to_string(need) +
+                                     " bytes of scratch; the library-resident scratch holds " +
+                                     std::to_string(ee::kScratchBytes) + " (reduce max_seq)");
+  char* base = static_cast<char*>(c->scratch);
+  uint64_t** const ptrs[kTwParts] = {&p.h, &p.h_exit, &p.z, &p.q, &p.o, &p.a, &p.kvnew, &p.dec, &p.attn_part};
+  tw_bind(reinterpret_cast<uint64_t*>(base), off, ptrs);
+  p.tw_all = reinterpret_cast<uint64_t*>(base);
+  p.tw_words = static_cast<int64_t>(head_off / 8);
+  p.head_part = reinterpret_cast<float*>(base + head_off);
+  p.counters = reinterpret_cast<ee::Counters*>(base + ctr_off);
+  return EE_OK;
+}
+
+// Launch n steps (decode, or prompt positions when prefill) and wait. With
+// na set, the outputs go to the caller's device arrays and the working set
+// to the library-resident scratch: nothing is allocated.
 int run_steps(ee_ctx* c, float tau, int exit_layer, int n, const int32_t* d_force_tok,
-              const int32_t* d_force_exit, bool prefill, bool debug) {
+              const int32_t* d_force_exit, bool prefill, bool debug, const NoAlloc* na = nullptr) {
   int r;
-  if ((r = ensure_ring(c, n))) return r;
-  if ((r = ensure_pages(c, c->pos + n))) return r;
   DevParams p = make_params(c, tau, prefill ? 0 : exit_layer);
-  p.ring_tok = c->d_ring_tok; p.ring_exit = c->d_ring_exit;
-  p.ring_would = c->d_ring_would; p.ring_conf = c->d_ring_conf;
-  p.ring_mass = c->d_ring_mass;
+  if (na && (r = bind_scratch(c, p))) return r;
+  if (!na && (r = ensure_ring(c, n))) return r;
+  if ((r = ensure_pages(c, c->pos + n))) return r;
+  if (na) {
+    p.ring_tok = na->tok; p.ring_exit = na->exited; p.ring_conf = na->conf;
+    p.ring_would = nullptr; p.ring_mass = nullptr;
+  } else {
+    p.ring_tok = c->d_ring_tok; p.ring_exit = c->d_ring_exit;
+    p.ring_would = c->d_ring_would; p.ring_conf = c->d_ring_conf;
+    p.ring_mass = c->d_ring_mass;
+  }
   p.nucleus = c->nucleus && !prefill;
   p.force_tok = d_force_tok;
   p.force_exit = d_force_exit;
@@ -356,8 +402,13 @@ int run_steps(ee_ctx* c, float tau, int exit_layer, int n, const int32_t* d_forc
     p.dbg_logits_f = c->d_dbg_f;
   }
   // Clear the step record except next_token, the first step's input.
-  HIPCHK(c, hipMemsetAsync(reinterpret_cast<char*>(c->d_ctl) + offsetof(ee::StepCtl, exited), 0,
-                           offsetof(ee::StepCtl, pad) - offsetof(ee::StepCtl, exited), c->stream));
+  if (na) {
+    hipError_t ce = ee::launch_clear_step(c->d_ctl, c->stream);
+    if (ce != hipSuccess) return hip_fail(c, ce, "step record clear");
+  } else {
+    HIPCHK(c, hipMemsetAsync(reinterpret_cast<char*>(c->d_ctl) + offsetof(ee::StepCtl, exited), 0,
+                             offsetof(ee::StepCtl, pad) - offsetof(ee::StepCtl, exited), c->stream));
+  }
   HIPCHK(c, hipEventRecord(c->ev0, c->stream));
   hipError_t e;
   const bool pers = c->persistent && c->nwg_persistent > 0 && c->slot >= 0;
@@ -589,6 +640,8 @@ static int create_body(ee_ctx* c, const ee_config* cfg, void* hip_stream, ee_ctx
   if ((he = hipGetDevice(&c->device)) != hipSuccess) return bail(hip_fail(c, he, "hipGetDevice"));
   if ((he = hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, c->device)) != hipSuccess)
     return bail(hip_fail(c, he, "hipDeviceGetAttribute"));
+  if ((he = ee::scratch_address(c->device, &c->scratch)) != hipSuccess)
+    return bail(hip_fail(c, he, "hipGetSymbolAddress of the library scratch"));
   if (hip_stream) {
     c->stream = static_cast<hipStream_t>(hip_stream);
   } else {
@@ -751,6 +804,20 @@ static int decode_n_ex_impl(ee_ctx* c, float tau, int32_t exit_layer, int32_t n,
 static int decode_n_impl(ee_ctx* c, float tau, int32_t exit_layer, int32_t n, int32_t* tokens,
                 int32_t* exited, float* conf) {
   return ee_decode_n_ex(c, tau, exit_layer, n, nullptr, nullptr, tokens, exited, conf, nullptr);
+}
+
+static int decode_n_noalloc_impl(ee_ctx* c, float tau, int32_t exit_layer, int32_t n, int32_t* d_tokens,
+                                 int32_t* d_exited, float* d_conf) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  if (n <= 0) return fail(c, EE_EINVAL, "n must be positive");
+  if (!d_tokens || !d_exited || !d_conf) return fail(c, EE_EINVAL, "output arrays must be non-null device pointers");
+  int r;
+  if ((r = check_gate_args(c, tau, exit_layer))) return r;
+  if (!c->have_next) return fail(c, EE_ESTATE, "no input token: run ee_prefill first");
+  if (!c->scratch) return fail(c, EE_ESTATE, "no library scratch on this device");
+  const NoAlloc na{d_tokens, d_exited, d_conf};
+  return run_steps(c, tau, exit_layer, n, nullptr, nullptr, false, false, &na);
 }
 
 static int decode_step_impl(ee_ctx* c, float tau, int32_t exit_layer, int32_t* out_token,
@@ -1148,6 +1215,10 @@ int ee_decode_n_ex(ee_ctx* c, float tau, int32_t exit_layer, int32_t n, const in
 int ee_decode_n(ee_ctx* c, float tau, int32_t exit_layer, int32_t n, int32_t* tokens,
                 int32_t* exited, float* conf) {
   return guarded(c, [&]() { return decode_n_impl(c, tau, exit_layer, n, tokens, exited, conf); });
+}
+int ee_decode_n_noalloc(ee_ctx* c, float tau, int32_t exit_layer, int32_t n, int32_t* d_tokens,
+                        int32_t* d_exited, float* d_conf) {
+  return guarded(c, [&]() { return decode_n_noalloc_impl(c, tau, exit_layer, n, d_tokens, d_exited, d_conf); });
 }
 int ee_decode_step(ee_ctx* c, float tau, int32_t exit_layer, int32_t* out_token,
                    int32_t* out_exited, float* out_conf) {

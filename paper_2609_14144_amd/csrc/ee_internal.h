@@ -16,6 +16,8 @@ constexpr int kMaxHeadDim = 256;
 constexpr int kBarGroups = 8;          // first level of the grid barrier (one per XCD)
 constexpr int kParamSlots = 16;        // persistent-kernel parameter blocks per device
 constexpr int kMaxPending = 8;         // exit-layer states a lazy fill batches at most
+constexpr size_t kScratchBytes = size_t(4) << 20;  // library-resident scratch per device
+constexpr int kMaxDevices = 64;
 constexpr int kStatFloats = 6;         // a head partial (max, sum, second max, argmax, entropy term, mass ahead)
 
 // Per-layer device pointers, repacked layouts:
@@ -112,7 +114,7 @@ struct DevParams {
   // per-call ring (device arrays of n)
   int32_t* ring_tok;
   int32_t* ring_exit;
-  int32_t* ring_would;
+  int32_t* ring_would;          // may be null
   float* ring_conf;
   float* ring_mass;             // full-head mass ahead of the readout token (when nucleus)
   int nucleus;                  // the final head also measures the readout token's nucleus rank
@@ -149,8 +151,13 @@ hipError_t launch_prefill_per_op(const DevParams& p, int wbf16, int pos0, const 
 hipError_t launch_prefill_persistent(const PersistentLaunch& L, int pos0, int n);
 hipError_t launch_head_eval(const DevParams& p, int wbf16, const float* d_x, int readout,
                             int head_wgs, hipStream_t s);
+// clear the per-call fields of the step record (all but next_token)
+hipError_t launch_clear_step(StepCtl* c, hipStream_t s);
 // copy the fp32 values of n tagged words to dst (device)
 hipError_t launch_untag(float* dst, const uint64_t* src, int n, hipStream_t s);
+// Device address of the library-resident scratch array (kScratchBytes) on
+// `device`, which must be the current device; looked up once per device.
+hipError_t scratch_address(int device, void** out);
 size_t lds_bytes(const DevParams& p);
 int fill_batch_slots(const DevParams& p);  // exit-layer states one lazy fill can batch
 int chunks_per_lane(const DevParams& p, int wbf16);

@@ -37,6 +37,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "ee_internal.h"
@@ -1460,7 +1461,7 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
           p.ring_tok[step] = idx;
           p.ring_exit[step] = 1;
           p.ring_conf[step] = conf;
-          p.ring_would[step] = would;
+          if (p.ring_would) p.ring_would[step] = would;
         }
       }
     } else {
@@ -1482,7 +1483,7 @@ __device__ void phase_head(const DevParams& p, int readout, int step, int wg, in
         p.ring_tok[step] = idx;
         p.ring_exit[step] = 0;
         p.ring_conf[step] = rconf;
-        p.ring_would[step] = rwould;
+        if (p.ring_would) p.ring_would[step] = rwould;
         if (nj >= 0 && p.ring_mass) p.ring_mass[step] = fin.a / fin.s;
       }
     }
@@ -2020,12 +2021,65 @@ __global__ __launch_bounds__(kWG) void k_reset_state(Counters* c, uint64_t* tw, 
     tw[i] = 0ull;
 }
 
+// The per-call fields of the step record (everything but next_token, the
+// first step's input), cleared by a kernel rather than a memset node.
+__global__ __launch_bounds__(64) void k_clear_step(StepCtl* c) {
+  if (threadIdx.x == 0) {
+    c->exited = 0;
+    c->would_exit = 0;
+    c->readout_token = 0;
+    c->full_token = 0;
+    c->conf = 0.f;
+    c->conf_full = 0.f;
+    c->error = 0;
+    c->abort = 0u;
+  }
+}
+
+hipError_t launch_clear_step(StepCtl* c, hipStream_t s) {
+  hipLaunchKernelGGL(k_clear_step, dim3(1), dim3(64), 0, s, c);
+  return hipGetLastError();
+}
+
 __global__ __launch_bounds__(kWG) void k_tag_vec(uint64_t* dst, const float* src, int n) {
   for (int i = blockIdx.x * kWG + threadIdx.x; i < n; i += gridDim.x * kWG) dst[i] = tw_pack(src[i], 0u);
 }
 
 __global__ __launch_bounds__(kWG) void k_untag(float* dst, const uint64_t* src, int n) {
   for (int i = blockIdx.x * kWG + threadIdx.x; i < n; i += gridDim.x * kWG) dst[i] = tw_val(src[i]);
+}
+
+// ---------------------------------------------------------------------------
+// Library-resident scratch for the allocation-free decode entry point: the
+// working set of a decode call (tagged activation words, attention and head
+// partial records, barrier counters) placed in a fixed device array instead
+// of memory the context allocates. Each device holds its own copy at its own
+// address; host code never passes the array's name to a kernel, only the
+// address hipGetSymbolAddress returns for the device that was current.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t scratch_address(int device, void** out) {
+  *out = nullptr;
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[device]) {
+    int cur = -1;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return e;
+    if (cur != device) return hipErrorInvalidDevice;  // the caller makes the device current
+    void* a = nullptr;
+    e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_addr[device] = a;
+  }
+  *out = g_scratch_addr[device];
+  return hipSuccess;
 }
 
 hipError_t launch_untag(float* dst, const uint64_t* src, int n, hipStream_t s) {
