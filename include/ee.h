@@ -236,11 +236,23 @@ int ee_calibration_record(ee_ctx* ctx, int32_t n, float* confs, float* masses);
 /* Periodic full-depth refresh (Section 11): recompute the cache entries of
  * the n most recent positions at every layer from their own input tokens,
  * replacing the entries projected for exited tokens by the KV-absence fill.
- * Runs the prompt program (full depth, ungated) over those positions, one
- * position after another: it costs n full-depth steps. The position and the
- * next input token are unchanged. Errors: EE_EINVAL (n outside
+ * Runs the full-depth pass of the prompt over those positions, batched (see
+ * ee_set_prefill_chunk): every weight is read once for all n positions. The
+ * position and the next input token are unchanged. Errors: EE_EINVAL (n outside
  * 1..position), EE_ESTATE, EE_EHIP, EE_EDEVICE. */
 int ee_refresh(ee_ctx* ctx, int32_t n);
+
+/* How full-depth passes over many positions run (ee_prefill, ee_refresh):
+ * positions > 0 batches chunks of at most that many positions (capped at
+ * 1024, and the default) through each layer together, so every weight is
+ * read once per chunk: per layer a tiled matrix product for the query, key
+ * and value projections (with RoPE and the cache stores), causal attention
+ * of the chunk's queries over every cached position up to their own, and
+ * matrix products for the output projection and the feed-forward block.
+ * 0 runs one position per step through the decode program (the earlier
+ * path; kept as a cross-check). Results agree to rounding (the summation
+ * order differs). Errors: EE_EINVAL (positions < 0). */
+int ee_set_prefill_chunk(ee_ctx* ctx, int32_t positions);
 
 /* EE_FILL_LAZY: in the persistent program an exit step only keeps its
  * exit-layer state; the cache entries of consecutive exited tokens are

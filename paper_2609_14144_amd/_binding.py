@@ -79,6 +79,7 @@ def _load():
         "ee_set_confidence_measure": (C.c_int, [V, C.c_int32]),
         "ee_refresh": (C.c_int, [V, C.c_int32]),
         "ee_set_fill_policy": (C.c_int, [V, C.c_int32]),
+        "ee_set_prefill_chunk": (C.c_int, [V, C.c_int32]),
         "ee_head_eval": (C.c_int, [V, C.c_int32, _FP, _IP, _FP, _FP]),
         "ee_read_kv": (C.c_int, [V, C.c_int32, C.c_int32, _FP, _FP]),
         "ee_set_persistent": (C.c_int, [V, C.c_int32]),
@@ -241,6 +242,10 @@ class Engine:
 
     def ee_set_fill_policy(self, policy: int):
         self._check(lib.ee_set_fill_policy(self._ctx, policy))
+
+    def ee_set_prefill_chunk(self, positions: int):
+        """0: one position per step (decode program); n > 0: batched chunks of n."""
+        self._check(lib.ee_set_prefill_chunk(self._ctx, int(positions)))
 
     def ee_refresh(self, n: int):
         self._check(lib.ee_refresh(self._ctx, n))

@@ -11,7 +11,7 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
-SOURCES = ["ee_api.hip", "ee_kernels.hip", "ee_probe.hip"]
+SOURCES = ["ee_api.hip", "ee_kernels.hip", "ee_batched.hip", "ee_probe.hip"]
 LIB = os.path.join(PKG, "libee.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <initializer_list>
 #include <atomic>
 #include <map>
 #include <new>
@@ -38,6 +39,9 @@ struct ee_ctx {
   float* g_final = nullptr;
   std::map<int, std::pair<void*, float*>> readout;
   ee::LayerW* d_layers = nullptr;
+  std::vector<ee::LayerW> h_layers;   // the same pointers, host side (batched pass)
+  ee::BatchBuffers bbuf{};            // batched full-depth pass (prompt, refresh)
+  int prefill_chunk = -1;             // -1: batched in chunks of bbuf.max_positions; 0: one position per step
 
   void* kpool = nullptr;
   void* vpool = nullptr;
@@ -674,6 +678,7 @@ static int create_body(ee_ctx* c, const ee_config* cfg, void* hip_stream, ee_ctx
       lw[l] = ee::LayerW{c->wqkv[l], c->wo[l], c->wgu[l], c->wd[l], c->g_attn[l], c->g_mlp[l]};
     if ((he = hipMemcpy(c->d_layers, lw.data(), L * sizeof(ee::LayerW), hipMemcpyHostToDevice)) != hipSuccess)
       return bail(hip_fail(c, he, "hipMemcpy layer table"));
+    c->h_layers = lw;
   }
   c->n_pages = (g.max_seq + g.page_size - 1) / g.page_size;
   c->layer_stride = static_cast<int64_t>(c->n_pages) * K * g.page_size * D;
@@ -712,6 +717,22 @@ static int create_body(ee_ctx* c, const ee_config* cfg, void* hip_stream, ee_ctx
     if ((he = hipMemset(c->d_tw, 0, total * 8)) != hipSuccess) return bail(hip_fail(c, he, "hipMemset"));
   }
   if ((r = dalloc(c, &c->d_hist, sizeof(int32_t) * g.max_seq))) return bail(r);
+  {
+    // chunks of up to 1024 positions: the residual stream, queries, attention
+    // output and feed-forward activations of a chunk, and the split workspaces
+    ee::BatchBuffers& b = c->bbuf;
+    const size_t Pm = static_cast<size_t>(std::min(1024, g.max_seq));
+    const size_t nmax = std::max({(A + 2 * K) * D, 2 * F, H});
+    b.max_positions = static_cast<int>(Pm);
+    b.gemm_ws_floats = std::min<size_t>(size_t(8) << 20, 32 * Pm * nmax);
+    b.attn_ws_floats = std::min<size_t>(size_t(8) << 20, 16 * Pm * A * (D + 2));
+    b.n_tile_ctr = ee::batch_tile_counters(static_cast<int>(Pm), static_cast<int>(nmax));
+    if ((r = dalloc(c, &b.X, Pm * H * 4)) || (r = dalloc(c, &b.Q, Pm * A * D * 4)) ||
+        (r = dalloc(c, &b.O, Pm * A * D * 4)) || (r = dalloc(c, &b.Act, Pm * F * 4)) ||
+        (r = dalloc(c, &b.gemm_ws, b.gemm_ws_floats * 4)) || (r = dalloc(c, &b.attn_ws, b.attn_ws_floats * 4)) ||
+        (r = dalloc(c, &b.tile_ctr, b.n_tile_ctr * 4)))
+      return bail(r);
+  }
   if ((r = dalloc(c, &c->d_counters, sizeof(ee::Counters)))) return bail(r);
   if ((r = dalloc(c, &c->d_ctl, sizeof(ee::StepCtl)))) return bail(r);
 
@@ -754,6 +775,45 @@ static int load_weights_impl(ee_ctx* c, const ee_tensor* tensors, int32_t n_tens
   return EE_OK;
 }
 
+// Full depth over positions pos .. pos + n - 1 with device input tokens
+// d_tokens, batched (chunks of positions through each layer together); with
+// head, the final head of the last position sets the next input token.
+// Advances the position; synchronous.
+static int batched_full_depth(ee_ctx* c, const int32_t* d_tokens, int n, bool head) {
+  int r;
+  if ((r = ensure_pages(c, c->pos + n))) return r;
+  ee::BatchPass bp{};
+  bp.p = make_params(c, INFINITY, 0);
+  bp.layers = c->h_layers.data();
+  bp.buf = c->bbuf;
+  if (c->prefill_chunk > 0) bp.buf.max_positions = std::min(c->prefill_chunk, c->bbuf.max_positions);
+  bp.wbf16 = c->wbf16;
+  bp.n_cu = c->n_cu;
+  HIPCHK(c, hipMemsetAsync(reinterpret_cast<char*>(c->d_ctl) + offsetof(ee::StepCtl, exited), 0,
+                           offsetof(ee::StepCtl, pad) - offsetof(ee::StepCtl, exited), c->stream));
+  HIPCHK(c, hipEventRecord(c->ev0, c->stream));
+  hipError_t e = ee::launch_batched_pass(bp, c->pos, d_tokens, n, c->stream);
+  if (e != hipSuccess) return hip_fail(c, e, "batched pass launch");
+  if (head) {
+    const int Pm = bp.buf.max_positions;
+    const int last = (n - 1) % Pm;  // row of the last position in the last chunk
+    e = ee::launch_head_eval(make_params(c, INFINITY, 0), c->wbf16,
+                             bp.buf.X + static_cast<size_t>(last) * c->cfg.hidden, 0, c->head_wgs, c->stream);
+    if (e != hipSuccess) return hip_fail(c, e, "prompt head launch");
+  }
+  HIPCHK(c, hipEventRecord(c->ev1, c->stream));
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  HIPCHK(c, hipEventElapsedTime(&c->last_ms, c->ev0, c->ev1));
+  ee::StepCtl ctl;
+  HIPCHK(c, hipMemcpy(&ctl, c->d_ctl, sizeof(ctl), hipMemcpyDeviceToHost));
+  if (ctl.error != ee::kErrNone) {
+    c->have_next = false;
+    return fail(c, EE_EDEVICE, "device: token id out of range");
+  }
+  c->pos += n;
+  return EE_OK;
+}
+
 static int prefill_impl(ee_ctx* c, const int32_t* tokens, int32_t n, int32_t* out_first_token) {
   if (!c) return EE_EINVAL;
   c->err.clear();
@@ -761,9 +821,14 @@ static int prefill_impl(ee_ctx* c, const int32_t* tokens, int32_t n, int32_t* ou
   if (!tokens || n <= 0) return fail(c, EE_EINVAL, "prefill needs at least one token");
   int r;
   if ((r = upload_force(c, n, tokens, nullptr))) return r;
-  if ((r = run_steps(c, INFINITY, 0, n, c->d_force_tok, nullptr, true, false))) return r;
+  if (c->prefill_chunk != 0) {
+    if ((r = batched_full_depth(c, c->d_force_tok, n, true))) return r;
+    c->have_next = true;
+  } else if ((r = run_steps(c, INFINITY, 0, n, c->d_force_tok, nullptr, true, false))) {
+    return r;
+  }
   int32_t tok = -1;
-  HIPCHK(c, hipMemcpy(&tok, c->d_ring_tok + (n - 1), sizeof(tok), hipMemcpyDeviceToHost));
+  HIPCHK(c, hipMemcpy(&tok, &c->d_ctl->next_token, sizeof(tok), hipMemcpyDeviceToHost));
   if (out_first_token) *out_first_token = tok;
   return EE_OK;
 }
@@ -781,7 +846,8 @@ static int refresh_impl(ee_ctx* c, int32_t n) {
   HIPCHK(c, hipMemcpy(&next, &c->d_ctl->next_token, sizeof(next), hipMemcpyDeviceToHost));
   const bool had = c->have_next;
   c->pos -= n;
-  r = run_steps(c, INFINITY, 0, n, c->d_force_tok, nullptr, true, false);
+  r = c->prefill_chunk != 0 ? batched_full_depth(c, c->d_force_tok, n, false)
+                            : run_steps(c, INFINITY, 0, n, c->d_force_tok, nullptr, true, false);
   if (r) {
     c->pos += n;
     c->have_next = false;
@@ -958,6 +1024,14 @@ static int set_readout_bias_impl(ee_ctx* c, int32_t exit_layer, const float* b, 
   if (it == c->readout.end() || !b) return fail(c, EE_EINVAL, "no readout at that layer");
   HIPCHK(c, hipMemcpyAsync(it->second.second, b, sizeof(float) * c->cfg.hidden,
                            on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice, c->stream));
+  return EE_OK;
+}
+
+static int set_prefill_chunk_impl(ee_ctx* c, int32_t positions) {
+  if (!c) return EE_EINVAL;
+  c->err.clear();
+  if (positions < 0) return fail(c, EE_EINVAL, "positions must be >= 0");
+  c->prefill_chunk = positions == 0 ? 0 : std::min(positions, c->bbuf.max_positions);
   return EE_OK;
 }
 
@@ -1184,6 +1258,8 @@ static void destroy_impl(ee_ctx* c) {
   dfree(c->d_ring_tok); dfree(c->d_ring_exit); dfree(c->d_ring_would); dfree(c->d_ring_conf); dfree(c->d_ring_mass);
   dfree(c->d_force_tok); dfree(c->d_force_exit); dfree(c->d_dbg_r); dfree(c->d_dbg_f);
   dfree(c->d_timeline);
+  dfree(c->bbuf.X); dfree(c->bbuf.Q); dfree(c->bbuf.O); dfree(c->bbuf.Act);
+  dfree(c->bbuf.gemm_ws); dfree(c->bbuf.attn_ws); dfree(c->bbuf.tile_ctr);
   if (c->ev0) (void)hipEventDestroy(c->ev0);
   if (c->ev1) (void)hipEventDestroy(c->ev1);
   if (c->own_stream && c->stream) (void)hipStreamDestroy(c->stream);
@@ -1238,6 +1314,9 @@ int ee_calibration_record(ee_ctx* c, int32_t n, float* confs, float* masses) {
 }
 int ee_set_readout_bias(ee_ctx* c, int32_t exit_layer, const float* b, int32_t on_device) {
   return guarded(c, [&]() { return set_readout_bias_impl(c, exit_layer, b, on_device); });
+}
+int ee_set_prefill_chunk(ee_ctx* c, int32_t positions) {
+  return guarded(c, [&]() { return set_prefill_chunk_impl(c, positions); });
 }
 int ee_set_fill_policy(ee_ctx* c, int32_t policy) {
   return guarded(c, [&]() { return set_fill_policy_impl(c, policy); });

@@ -132,6 +132,37 @@ struct DevParams {
   int timeline_cap;  // entries
 };
 
+// Buffers of the batched full-depth pass (ee_batched.hip), owned by the
+// context and sized for chunks of at most max_positions positions.
+struct BatchBuffers {
+  int max_positions;
+  float* X;               // [max_positions][H] residual stream
+  float* Q;               // [max_positions][A*D] queries after RoPE
+  float* O;               // [max_positions][A*D] attention output
+  float* Act;             // [max_positions][F] SiLU(gate) * up
+  float* gemm_ws;         // split-K partial sums
+  size_t gemm_ws_floats;
+  uint32_t* tile_ctr;     // arrivals per output tile (zero between launches)
+  size_t n_tile_ctr;
+  float* attn_ws;         // attention partial records of key splits
+  size_t attn_ws_floats;
+};
+
+struct BatchPass {
+  DevParams p;            // shapes, embedding, cache, RoPE tables, block table, token history, step record
+  const LayerW* layers;   // host array [L] of the layers' device pointers
+  BatchBuffers buf;
+  int wbf16;
+  int n_cu;
+};
+
+// Full depth over positions pos0 .. pos0 + n - 1 with input tokens d_tokens
+// (device), in chunks of buf.max_positions: every layer's cache entries of
+// those positions; the residual stream of the last chunk stays in buf.X.
+hipError_t launch_batched_pass(const BatchPass& bp, int pos0, const int32_t* d_tokens, int n, hipStream_t s);
+// tile counters the pass needs for chunks of max_positions and outputs of at most N_max rows
+size_t batch_tile_counters(int max_positions, int N_max);
+
 // Host launchers (defined in ee_kernels.hip).
 hipError_t launch_decode_per_op(const DevParams& p, int wbf16, int pos0, int n, int head_wgs,
                                 hipStream_t s);

@@ -356,6 +356,70 @@ def test_refresh_recomputes_the_cache(persistent):
             e.ee_refresh(n)
 
 
+@pytest.mark.parametrize("chunk", [None, 7, 0], ids=["batched", "chunks_of_7", "stepwise"])
+@pytest.mark.parametrize("name", ["tiny", "tiny_bf16"])
+def test_prompt_pass_matches_oracle(name, chunk):
+    """The prompt pass batched over positions (the default chunks, and chunks
+    of 7 positions, whose later chunks attend to the earlier ones through
+    the cache) and one position per step through the decode program: every
+    layer's cache entries of every prompt position and the first token
+    against the oracle's prompt pass, ragged lengths, then lockstep decode."""
+    cfg = synth.get_config(name)
+    for P in (1, 5, 16, 37, 200):
+        prompt = synth.prompts(cfg, 60 + P, P)
+        o = oracle_for(name, P + 4)
+        g0 = o.prefill(prompt)
+        e = engine(name, P + 4, page_size=16)
+        if chunk is not None:
+            e.ee_set_prefill_chunk(chunk)
+        g = e.ee_prefill(prompt)
+        if o.last_prefill_stats[2] > MARGIN:
+            assert g == g0, (P, g, g0)
+        assert e.ee_position() == P
+        check_kv(e, o, cfg, range(cfg.n_layers), range(P))
+        lockstep(e, o, g0, 0.5, 2, 4, force_tokens=synth.prompts(cfg, 61 + P, 4), force_exit=[1, 0, 1, 0])
+        e.close()
+
+
+def test_prompt_pass_is_deterministic():
+    """Two batched prompt passes give identical cache bytes and tokens: the
+    split-K partial sums and the attention splits are added in a fixed
+    order whatever the scheduling."""
+    name = "tiny_bf16"
+    cfg = synth.get_config(name)
+    prompt = synth.prompts(cfg, 13, 300)
+    runs = []
+    for _ in range(2):
+        e = engine(name, 304, page_size=16)
+        g = e.ee_prefill(prompt)
+        runs.append((g, _kv_all(e, cfg, range(300))))
+        e.close()
+    assert runs[0][0] == runs[1][0]
+    np.testing.assert_array_equal(runs[0][1], runs[1][1])
+
+
+@pytest.mark.timeout(900)
+def test_d1p5b_refresh_matches_oracle(d15):
+    """The periodic full-depth refresh at the 1.5B shape (Section 11): after
+    16 imposed exits, ee_refresh(16) recomputes those positions' cache
+    entries at every layer as the oracle's refresh does (16 positions: the
+    matrix products split K over many workgroups at these shapes)."""
+    cfg, w, prompt, o, g0 = d15
+    o.reset()
+    o.prefill(prompt)
+    toks = synth.prompts(cfg, 21, 16)
+    o.generate(None, 0.3, 14, 16, force_tokens=toks, force_exit=np.ones(16, np.int32))
+    o.refresh(16)
+    e = engine(D15, 512 + 64)
+    e.ee_prefill(prompt)
+    _, ex, _, _ = e.ee_decode_n_ex(0.3, 14, 16, force_tokens=toks, force_exit=np.ones(16, np.int32))
+    assert ex.all()
+    e.ee_refresh(16)
+    assert e.ee_position() == 512 + 16
+    check_kv(e, o, cfg, [0, 7, 14, 20, 27], range(512, 528))
+    e.close()
+
+
 def _kv_all(e, cfg, positions):
     out = []
     for l in range(cfg.n_layers):
