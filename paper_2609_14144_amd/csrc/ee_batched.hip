@@ -112,15 +112,28 @@ __device__ __forceinline__ int64_t cache_off(const int32_t* block_table, int pag
   return layer_base + ((static_cast<int64_t>(page) * K + kvh) * page_size + slot) * D;
 }
 
+// Wave reductions: DPP within rows of 16 lanes, then the four row results
+// by readlane; every lane gets the same value, summed in a fixed order.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float lane_of(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
 __device__ __forceinline__ float wave_max64(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
+  v = fmaxf(v, dpp_mov<0xB1>(v));   // lane ^ 1
+  v = fmaxf(v, dpp_mov<0x4E>(v));   // lane ^ 2
+  v = fmaxf(v, dpp_mov<0x141>(v));  // the other quad of the 8
+  v = fmaxf(v, dpp_mov<0x140>(v));  // the other 8 of the 16
+  return fmaxf(fmaxf(lane_of(v, 0), lane_of(v, 16)), fmaxf(lane_of(v, 32), lane_of(v, 48)));
 }
 __device__ __forceinline__ float wave_sum64(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  v += dpp_mov<0xB1>(v);
+  v += dpp_mov<0x4E>(v);
+  v += dpp_mov<0x141>(v);
+  v += dpp_mov<0x140>(v);
+  return (lane_of(v, 0) + lane_of(v, 16)) + (lane_of(v, 32) + lane_of(v, 48));
 }
 
 }  // namespace
@@ -445,6 +458,397 @@ __global__ __launch_bounds__(256) void k_bp_gemm(GemmArgs g) {
 }
 
 // ---------------------------------------------------------------------------
+// The same product for bf16 weights on the matrix cores
+// (v_mfma_f32_16x16x32_bf16): 16 weight rows x 16 positions per MFMA. The
+// weights are exact bf16 operands; every fp32 activation x (times its gain)
+// is split exactly into three bf16 terms t1 + t2 + t3 (t1 its top 16 bits,
+// t2 those of the remainder, t3 the rest, which fits in 8 significant bits),
+// and the three products accumulate in fp32, so the result carries fp32
+// accumulation error only, as the vector-ALU product does.
+// Block: 4 waves, each RB row blocks of 16 rows; CP column blocks of 16
+// positions; K in steps of 64. Lane l (row / position l % 16, group
+// g = l / 16) loads 32 contiguous bytes of its row, k0 + 16 g .. + 15 (four
+// lanes read a whole 128-byte line); the low half feeds one MFMA whose k
+// slots (g, j) are k0 + 16 g + j, the high half a second with k0 + 16 g + 8
+// + j, and the activation operands in LDS are laid out to match.
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ bf16x8 as_bf16x8(const uint4& u) { return __builtin_bit_cast(bf16x8, u); }
+
+// three bf16 terms of each of four floats: term t of element i in 16 bits
+__device__ __forceinline__ void split3(const float4& x, uint2* t) {
+  const float v[4] = {x.x, x.y, x.z, x.w};
+  uint32_t b[3][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t u = __float_as_uint(v[i]);
+    const uint32_t h1 = u & 0xffff0000u;
+    const float r1 = v[i] - __uint_as_float(h1);
+    const uint32_t h2 = __float_as_uint(r1) & 0xffff0000u;
+    const float r2 = r1 - __uint_as_float(h2);
+    b[0][i] = h1 >> 16;
+    b[1][i] = h2 >> 16;
+    b[2][i] = __float_as_uint(r2) >> 16;  // exact: r2 has at most 8 significant bits
+  }
+#pragma unroll
+  for (int k = 0; k < 3; ++k) t[k] = make_uint2(b[k][0] | (b[k][1] << 16), b[k][2] | (b[k][3] << 16));
+}
+
+// NS > 0: the K-slice has at most NS steps and all its loads are issued
+// before the first product (few positions: each step has little arithmetic
+// to hide a load behind); NS = 0: the next step's loads fly during a step.
+template <int EPI, int RB, int CP, int NS>
+__global__ __launch_bounds__(256) void k_bp_gemm_mfma(GemmArgs g) {
+  constexpr int BN = 64 * RB, BP = 16 * CP, KS = 64;
+  constexpr int XCH = BP * KS / 4 / 256;  // float4 of activations per thread per step
+  // activation terms of one step, double buffered:
+  // [buf][term][column block][group][position][half] as 16-byte chunks
+  __shared__ uint4 Xs[2][3][CP][4][16][2];
+  __shared__ float ss_part[BP];
+  __shared__ int last_flag;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int lg = lane >> 4, lr = lane & 15;
+  const int n0 = blockIdx.x * BN, p0 = blockIdx.y * BP;
+  const int split = blockIdx.z, splits = gridDim.z;
+  const int kb = split * g.k_split, ke = min(g.K, kb + g.k_split);
+  const uint16_t* W = static_cast<const uint16_t*>(g.W);
+
+  float ssq[XCH];
+#pragma unroll
+  for (int i = 0; i < XCH; ++i) ssq[i] = 0.f;
+  float4 xr[XCH];
+  uint4 wr[RB][2];
+  auto load_w_into = [&](int k0, uint4 (&wr)[RB][2]) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int n = n0 + (wave * RB + rb) * 16 + lr;
+      const int k = k0 + 16 * lg;
+      const uint4* src = reinterpret_cast<const uint4*>(W + static_cast<int64_t>(n) * g.K + k);
+      wr[rb][0] = (n < g.N && k < ke) ? src[0] : make_uint4(0u, 0u, 0u, 0u);
+      wr[rb][1] = (n < g.N && k + 8 < ke) ? src[1] : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  auto load_x_into = [&](int k0, float4 (&xr)[XCH]) {
+#pragma unroll
+    for (int i = 0; i < XCH; ++i) {
+      const int c = tid + 256 * i;
+      const int p = c >> 4, k = k0 + 4 * (c & 15);
+      xr[i] = (p0 + p < g.P && k < ke)
+                  ? *reinterpret_cast<const float4*>(g.A + static_cast<int64_t>(p0 + p) * g.K + k)
+                  : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  auto store_x_from = [&](int buf, int k0, const float4 (&xr)[XCH]) {
+#pragma unroll
+    for (int i = 0; i < XCH; ++i) {
+      const int c = tid + 256 * i;
+      const int p = c >> 4, kq = c & 15, k = k0 + 4 * kq;
+      float4 a = xr[i];
+      if (g.gain) {
+        ssq[i] = fmaf(a.x, a.x, fmaf(a.y, a.y, fmaf(a.z, a.z, fmaf(a.w, a.w, ssq[i]))));
+        if (k < ke) {
+          const float4 gg = *reinterpret_cast<const float4*>(g.gain + k);
+          a.x *= gg.x; a.y *= gg.y; a.z *= gg.z; a.w *= gg.w;
+        }
+      }
+      uint2 t[3];
+      split3(a, t);
+      const int grp = kq >> 2, j0 = 4 * (kq & 3);  // k - k0 = 16 grp + j0
+#pragma unroll
+      for (int term = 0; term < 3; ++term) {
+        uint2* dst = reinterpret_cast<uint2*>(&Xs[buf][term][p >> 4][grp][p & 15][j0 >> 3]) + ((j0 >> 2) & 1);
+        *dst = t[term];
+      }
+    }
+  };
+
+  f32x4 acc[RB][CP];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int cp = 0; cp < CP; ++cp) acc[rb][cp] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto products = [&](int buf, const uint4 (&wc)[RB][2]) {
+#pragma unroll
+    for (int cp = 0; cp < CP; ++cp) {
+#pragma unroll
+      for (int term = 0; term < 3; ++term) {
+        const bf16x8 blo = as_bf16x8(Xs[buf][term][cp][lg][lr][0]);
+        const bf16x8 bhi = as_bf16x8(Xs[buf][term][cp][lg][lr][1]);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          acc[rb][cp] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(wc[rb][0]), blo, acc[rb][cp], 0, 0, 0);
+          acc[rb][cp] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(wc[rb][1]), bhi, acc[rb][cp], 0, 0, 0);
+        }
+      }
+    }
+  };
+
+  if constexpr (NS > 0) {
+    // the whole K-slice's loads first
+    const int nst = (ke - kb + KS - 1) / KS;
+    uint4 wall[NS][RB][2];
+    float4 xall[NS][XCH];
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+      if (st < nst) {
+        load_w_into(kb + st * KS, wall[st]);
+        load_x_into(kb + st * KS, xall[st]);
+      }
+    }
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+      if (st < nst) {
+        store_x_from(st & 1, kb + st * KS, xall[st]);
+        __syncthreads();
+        products(st & 1, wall[st]);
+      }
+    }
+  } else {
+    int buf = 0;
+    if (kb < ke) {
+      load_w_into(kb, wr);
+      load_x_into(kb, xr);
+    }
+    for (int k0 = kb; k0 < ke; k0 += KS) {
+      store_x_from(buf, k0, xr);
+      __syncthreads();
+      uint4 wc[RB][2];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        wc[rb][0] = wr[rb][0];
+        wc[rb][1] = wr[rb][1];
+      }
+      if (k0 + KS < ke) {  // the next step's loads fly during this step's products
+        load_w_into(k0 + KS, wr);
+        load_x_into(k0 + KS, xr);
+      }
+      products(buf, wc);
+      buf ^= 1;  // the other buffer is written next; this one is read until the barrier after that store
+    }
+  }
+
+  // per-position sums of squares of this K-slice: the 16 threads of a
+  // position are consecutive lanes
+  if (g.gain) {
+#pragma unroll
+    for (int i = 0; i < XCH; ++i) {
+      float v = ssq[i];
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) v += __shfl_xor(v, o);
+      const int c = tid + 256 * i;
+      if ((c & 15) == 0) ss_part[c >> 4] = v;
+    }
+  }
+  __syncthreads();
+
+  // lane's outputs: rows n0 + (wave RB + rb) 16 + 4 lg + i (i < 4), position p0 + 16 cp + lr
+  const int64_t PN = static_cast<int64_t>(g.P) * g.N;
+  if (splits > 1) {
+    float* part = g.part + split * PN;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int cp = 0; cp < CP; ++cp) {
+        const int n = n0 + (wave * RB + rb) * 16 + 4 * lg, p = p0 + 16 * cp + lr;
+        if (n < g.N && p < g.P) {
+          float* d = part + static_cast<int64_t>(p) * g.N + n;
+          st_agent2(d, acc[rb][cp][0], acc[rb][cp][1]);
+          st_agent2(d + 2, acc[rb][cp][2], acc[rb][cp][3]);
+        }
+      }
+    if (g.gain && tid < BP && p0 + tid < g.P) st_agent(g.part + splits * PN + split * g.P + p0 + tid, ss_part[tid]);
+    drain_stores();
+    __syncthreads();
+    if (tid == 0) {
+      uint32_t* ctr = g.tile_ctr + blockIdx.y * gridDim.x + blockIdx.x;
+      const uint32_t old = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      last_flag = old == static_cast<uint32_t>(splits - 1);
+      if (last_flag) __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    if (!last_flag) return;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int cp = 0; cp < CP; ++cp) acc[rb][cp] = f32x4{0.f, 0.f, 0.f, 0.f};
+    constexpr int kSG = (RB * CP >= 4) ? 1 : 16;  // slices with loads in flight together
+    for (int s0 = 0; s0 < splits; s0 += kSG) {
+      float2 v[kSG][RB][CP][2];
+#pragma unroll
+      for (int u = 0; u < kSG; ++u)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+          for (int cp = 0; cp < CP; ++cp) {
+            const int n = n0 + (wave * RB + rb) * 16 + 4 * lg, p = p0 + 16 * cp + lr;
+            const bool ok = s0 + u < splits && n < g.N && p < g.P;
+            const float* d = g.part + (s0 + u) * PN + static_cast<int64_t>(p) * g.N + n;
+            v[u][rb][cp][0] = ok ? ld_agent2(d) : make_float2(0.f, 0.f);
+            v[u][rb][cp][1] = ok ? ld_agent2(d + 2) : make_float2(0.f, 0.f);
+          }
+#pragma unroll
+      for (int u = 0; u < kSG; ++u)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+          for (int cp = 0; cp < CP; ++cp) {
+            acc[rb][cp][0] += v[u][rb][cp][0].x;
+            acc[rb][cp][1] += v[u][rb][cp][0].y;
+            acc[rb][cp][2] += v[u][rb][cp][1].x;
+            acc[rb][cp][3] += v[u][rb][cp][1].y;
+          }
+    }
+    if (g.gain && tid < BP && p0 + tid < g.P) {
+      float t = 0.f;
+      for (int s0 = 0; s0 < splits; s0 += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          v[u] = s0 + u < splits ? ld_agent(g.part + splits * PN + (s0 + u) * g.P + p0 + tid) : 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) t += v[u];
+      }
+      ss_part[tid] = t;
+    }
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int cp = 0; cp < CP; ++cp) {
+    const int pl = 16 * cp + lr, p = p0 + pl;
+    if (p >= g.P) continue;
+    const float rinv = g.gain ? rsqrtf(ss_part[pl] / static_cast<float>(g.K) + g.eps) : 1.f;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int n = n0 + (wave * RB + rb) * 16 + 4 * lg;
+      if (n < g.N) epi_pair<uint16_t>(g, EPI, p, n, acc[rb][cp][0] * rinv, acc[rb][cp][1] * rinv);
+      if (n + 2 < g.N) epi_pair<uint16_t>(g, EPI, p, n + 2, acc[rb][cp][2] * rinv, acc[rb][cp][3] * rinv);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Few positions (P <= 16) on the matrix cores without a cross-workgroup
+// merge: a workgroup owns RB x 16 weight rows and all 16 positions, its NW
+// waves split K into contiguous ranges of 64-wide steps, and the waves' sums
+// meet in LDS in wave order. Lane l (row / position l % 16, group l / 16)
+// loads its own operands straight into registers: 32 bytes of its weight
+// row, 16 activations of its position (and their gains), the same k range
+// k0 + 16 (l / 16) .. + 15 as above; a ring of PF steps is in flight.
+// ---------------------------------------------------------------------------
+template <int EPI, int RB, int NW, int PF>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_bp_gemm_narrow(GemmArgs g) {
+  constexpr int KS = 64;
+  constexpr bool kGain = EPI != kEpiResid;  // the gated products normalise their input
+  __shared__ f32x4 red[NW][RB][64];
+  __shared__ float ssr[NW][64];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int lg = lane >> 4, lr = lane & 15;
+  const int n0 = blockIdx.x * 16 * RB;
+  const int nsteps = (g.K + KS - 1) / KS;
+  const int s0 = nsteps * wave / NW, s1 = nsteps * (wave + 1) / NW;
+  const bool pok = lr < g.P;
+  const uint16_t* W = static_cast<const uint16_t*>(g.W);
+  const float* xrow = g.A + static_cast<int64_t>(lr) * g.K;
+
+  uint4 wr[PF][RB][2];
+  float4 xr[PF][4];
+  float4 gr[kGain ? PF : 1][4];
+  auto load = [&](int st, int slot) {
+    const int k = st * KS + 16 * lg;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int row = n0 + rb * 16 + lr;
+      const uint4* src = reinterpret_cast<const uint4*>(W + static_cast<int64_t>(row) * g.K + k);
+      wr[slot][rb][0] = (row < g.N && k < g.K) ? src[0] : make_uint4(0u, 0u, 0u, 0u);
+      wr[slot][rb][1] = (row < g.N && k + 8 < g.K) ? src[1] : make_uint4(0u, 0u, 0u, 0u);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const bool ok = k + 4 * q < g.K;
+      xr[slot][q] = (pok && ok) ? *reinterpret_cast<const float4*>(xrow + k + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+      if constexpr (kGain)
+        gr[slot][q] = ok ? *reinterpret_cast<const float4*>(g.gain + k + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  f32x4 acc[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float ssq = 0.f;
+#pragma unroll
+  for (int i = 0; i < PF; ++i)
+    if (s0 + i < s1) load(s0 + i, i);
+  for (int st = s0; st < s1; st += PF) {
+#pragma unroll
+    for (int i = 0; i < PF; ++i) {
+      if (st + i < s1) {
+        float4 x[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          x[q] = xr[i][q];
+          if constexpr (kGain) {
+            ssq = fmaf(x[q].x, x[q].x, fmaf(x[q].y, x[q].y, fmaf(x[q].z, x[q].z, fmaf(x[q].w, x[q].w, ssq))));
+            x[q].x *= gr[i][q].x; x[q].y *= gr[i][q].y; x[q].z *= gr[i][q].z; x[q].w *= gr[i][q].w;
+          }
+        }
+        // three bf16 terms of the low (k .. k + 7) and high (k + 8 .. + 15) halves
+        uint2 t[4][3];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) split3(x[q], t[q]);
+        uint4 wc[RB][2];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          wc[rb][0] = wr[i][rb][0];
+          wc[rb][1] = wr[i][rb][1];
+        }
+        if (st + i + PF < s1) load(st + i + PF, i);  // refill the slot just read
+#pragma unroll
+        for (int term = 0; term < 3; ++term) {
+          const uint4 blo = make_uint4(t[0][term].x, t[0][term].y, t[1][term].x, t[1][term].y);
+          const uint4 bhi = make_uint4(t[2][term].x, t[2][term].y, t[3][term].x, t[3][term].y);
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(wc[rb][0]), as_bf16x8(blo), acc[rb], 0, 0, 0);
+            acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(wc[rb][1]), as_bf16x8(bhi), acc[rb], 0, 0, 0);
+          }
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) red[wave][rb][lane] = acc[rb];
+  ssr[wave][lane] = ssq;
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    f32x4 t = red[0][rb][lane];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) t += red[w][rb][lane];
+    acc[rb] = t;
+  }
+  float rinv = 1.f;
+  if constexpr (kGain) {
+    // position lr's sum of squares: the four lane groups of every wave
+    float t = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+      t += (ssr[w][lr] + ssr[w][lr + 16]) + (ssr[w][lr + 32] + ssr[w][lr + 48]);
+    rinv = rsqrtf(t / static_cast<float>(g.K) + g.eps);
+  }
+  if (!pok) return;
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int n = n0 + rb * 16 + 4 * lg;
+    if (n < g.N) epi_pair<uint16_t>(g, EPI, lr, n, acc[rb][0] * rinv, acc[rb][1] * rinv);
+    if (n + 2 < g.N) epi_pair<uint16_t>(g, EPI, lr, n + 2, acc[rb][2] * rinv, acc[rb][3] * rinv);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // causal grouped-query attention of a chunk of queries (positions pos0 ..
 // pos0 + P - 1) over the cache. Block = (KV head, tile of 4 query
 // positions, key split); wave w takes query position 4 t + w with the G query
@@ -470,16 +874,18 @@ struct AttnArgs {
 constexpr int kQT = 4;   // query positions per block (one per wave)
 constexpr int kKT = 64;  // keys per LDS tile
 
-template <typename WT, int D>
-__global__ __launch_bounds__(256) void k_bp_attn(AttnArgs a) {
+// At most two workgroups fit per compute unit by LDS, so each wave may hold
+// up to 256 registers (two waves per SIMD).
+template <typename WT, int D, int G>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_bp_attn(AttnArgs a) {
   constexpr int EPC = St<WT>::N;
   constexpr int CPK = D / EPC;          // 16-byte chunks per cache row
   constexpr int DPL = D / 64;           // output dimensions per lane (1 or 2)
   constexpr int KST = CPK + 1;          // key rows padded by one chunk: lane j reads row j
   __shared__ uint4 Ks[kKT * KST];
   __shared__ uint4 Vs[kKT * CPK];
-  __shared__ float Qs[kQT][kMaxGroup][D];
-  __shared__ float Ps[kQT][kMaxGroup][kKT];
+  __shared__ float Qs[kQT][G][D];
+  __shared__ float Ps[kQT][G][kKT];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int nqt = (a.P + kQT - 1) / kQT;
@@ -487,7 +893,6 @@ __global__ __launch_bounds__(256) void k_bp_attn(AttnArgs a) {
   const int kvh = item / (nqt * a.nsplit);
   const int rem = item - kvh * nqt * a.nsplit;
   const int qt = rem / a.nsplit, sp = rem - qt * a.nsplit;
-  const int G = a.G;
   const int qi = qt * kQT + wave;               // query index within the chunk
   const bool active = qi < a.P;
   const int qpos = a.pos0 + qi;                 // its position
@@ -495,14 +900,28 @@ __global__ __launch_bounds__(256) void k_bp_attn(AttnArgs a) {
   const int kb = sp * a.keys_per_split;
   const int ke = min(t_end, kb + a.keys_per_split);
 
-  // the wave's query rows (G heads of this KV head), every load in flight at once
+  constexpr int CPT = kKT * CPK / 256;  // chunks of K (and of V) per thread per tile
+  // cache offsets of a tile's chunks (its page lookups)
+  auto offsets = [&](int k0, int64_t (&off)[CPT]) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = tid + 256 * i;
+      const int j = c / CPK, q = c - j * CPK;
+      const int key = min(k0 + j, ke - 1);
+      off[i] = cache_off(a.block_table, a.page_shift, a.page_size, a.K, D, a.layer_base, key, kvh) + q * EPC;
+    }
+  };
+  // the wave's query rows (the G heads of this KV head) and the first tile's
+  // page lookups, every load in flight at once
+  int64_t off[CPT];
+  if (kb < ke) offsets(kb, off);
   {
-    constexpr int QPL = kMaxGroup * D / 64;
+    constexpr int QPL = G * D / 64;
     float qv[QPL];
 #pragma unroll
     for (int u = 0; u < QPL; ++u) {
       const int i = lane + 64 * u, h = i / D, d = i - h * D;
-      qv[u] = (active && h < G) ? a.Q[static_cast<int64_t>(qi) * a.A * D + (kvh * G + h) * D + d] : 0.f;
+      qv[u] = active ? a.Q[static_cast<int64_t>(qi) * a.A * D + (kvh * G + h) * D + d] : 0.f;
     }
 #pragma unroll
     for (int u = 0; u < QPL; ++u) {
@@ -510,9 +929,9 @@ __global__ __launch_bounds__(256) void k_bp_attn(AttnArgs a) {
       Qs[wave][h][d] = qv[u];
     }
   }
-  float m_run[kMaxGroup], l_run[kMaxGroup], acc[kMaxGroup][DPL];
+  float m_run[G], l_run[G], acc[G][DPL];
 #pragma unroll
-  for (int h = 0; h < kMaxGroup; ++h) {
+  for (int h = 0; h < G; ++h) {
     m_run[h] = -INFINITY;
     l_run[h] = 0.f;
 #pragma unroll
@@ -521,18 +940,8 @@ __global__ __launch_bounds__(256) void k_bp_attn(AttnArgs a) {
   const WT* kp = static_cast<const WT*>(a.kpool);
   const WT* vp = static_cast<const WT*>(a.vpool);
 
-  constexpr int CPT = kKT * CPK / 256;  // chunks of K (and of V) per thread per tile
   for (int k0 = kb; k0 < ke; k0 += kKT) {
-    // every page lookup of the tile, then every K and V load, before any
-    // result is waited for: two round trips per tile
-    int64_t off[CPT];
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + 256 * i;
-      const int j = c / CPK, q = c - j * CPK;
-      const int key = min(k0 + j, ke - 1);
-      off[i] = cache_off(a.block_table, a.page_shift, a.page_size, a.K, D, a.layer_base, key, kvh) + q * EPC;
-    }
+    if (k0 != kb) offsets(k0, off);
     uint4 kv[CPT], vv[CPT];
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
@@ -550,24 +959,21 @@ __global__ __launch_bounds__(256) void k_bp_attn(AttnArgs a) {
     __syncthreads();
     const int key = k0 + lane;
     const bool valid = active && key < ke && key <= qpos;
-    float s[kMaxGroup];
+    float s[G];
 #pragma unroll
-    for (int h = 0; h < kMaxGroup; ++h) s[h] = 0.f;
-#pragma unroll 4
+    for (int h = 0; h < G; ++h) s[h] = 0.f;
+#pragma unroll 2
     for (int q = 0; q < CPK; ++q) {
       float kf[EPC];
       St<WT>::unpack(Ks[lane * KST + q], kf);
 #pragma unroll
-      for (int h = 0; h < kMaxGroup; ++h) {
-        if (h < G) {
+      for (int h = 0; h < G; ++h) {
 #pragma unroll
-          for (int e = 0; e < EPC; ++e) s[h] = fmaf(Qs[wave][h][q * EPC + e], kf[e], s[h]);
-        }
+        for (int e = 0; e < EPC; ++e) s[h] = fmaf(Qs[wave][h][q * EPC + e], kf[e], s[h]);
       }
     }
 #pragma unroll
-    for (int h = 0; h < kMaxGroup; ++h) {
-      if (h >= G) continue;
+    for (int h = 0; h < G; ++h) {
       const float sv = valid ? s[h] * a.scale : -INFINITY;
       const float mt = wave_max64(sv);
       const float mn = fmaxf(m_run[h], mt);
@@ -584,7 +990,7 @@ __global__ __launch_bounds__(256) void k_bp_attn(AttnArgs a) {
     }
     __builtin_amdgcn_wave_barrier();
     // weighted values: lane owns dimensions DPL * lane .. + DPL - 1
-#pragma unroll 8
+#pragma unroll 4
     for (int j = 0; j < kKT; ++j) {
       float v[DPL];
       if constexpr (DPL == 2) {
@@ -597,19 +1003,16 @@ __global__ __launch_bounds__(256) void k_bp_attn(AttnArgs a) {
         else v[0] = vr[lane];
       }
 #pragma unroll
-      for (int h = 0; h < kMaxGroup; ++h) {
-        if (h < G) {
-          const float pj = Ps[wave][h][j];
+      for (int h = 0; h < G; ++h) {
+        const float pj = Ps[wave][h][j];
 #pragma unroll
-          for (int e = 0; e < DPL; ++e) acc[h][e] = fmaf(pj, v[e], acc[h][e]);
-        }
+        for (int e = 0; e < DPL; ++e) acc[h][e] = fmaf(pj, v[e], acc[h][e]);
       }
     }
   }
   if (!active) return;
 #pragma unroll
-  for (int h = 0; h < kMaxGroup; ++h) {
-    if (h >= G) continue;
+  for (int h = 0; h < G; ++h) {
     const int head = kvh * G + h;
     if (a.nsplit == 1) {
       const float inv = 1.f / l_run[h];
@@ -686,10 +1089,12 @@ namespace {
 // Splits of K so that the grid holds at least ~2 workgroups per compute unit,
 // bounded by the partial workspace and by one stage per split.
 void choose_split(int tiles, int P, int N, int K, int BK, size_t ws_floats, int wgs_per_cu, int n_cu, int* k_split,
-                  int* splits) {
+                  int* splits, int max_k_split = 1 << 30) {
   // enough workgroups per compute unit (wgs_per_cu) that their weight loads
-  // in flight together cover the memory latency; at most 32 slices
+  // in flight together cover the memory latency; at most 32 slices, and
+  // slices of at most max_k_split
   int s = std::max(1, (wgs_per_cu * n_cu + tiles - 1) / tiles);
+  s = std::max(s, (K + max_k_split - 1) / max_k_split);
   s = std::min({s, (K + BK - 1) / BK, 32});
   const size_t per = static_cast<size_t>(P) * N + P;
   if (per > 0) s = static_cast<int>(std::min<size_t>(s, std::max<size_t>(1, ws_floats / per)));
@@ -704,10 +1109,38 @@ void choose_split(int tiles, int P, int N, int K, int BK, size_t ws_floats, int 
   *splits = (K + ks - 1) / ks;
 }
 
+template <int EPI, int RB, int CP, int NS>
+hipError_t gemm_mfma(GemmArgs g, const BatchBuffers& b, int n_cu, int wgs_per_cu, hipStream_t s) {
+  constexpr int BN = 64 * RB, BP = 16 * CP;
+  const int tiles = ((g.N + BN - 1) / BN) * ((g.P + BP - 1) / BP);
+  if (static_cast<size_t>(tiles) > b.n_tile_ctr) return hipErrorInvalidValue;
+  int splits;
+  choose_split(tiles, g.P, g.N, g.K, 64, b.gemm_ws_floats, wgs_per_cu, n_cu, &g.k_split, &splits,
+               NS > 0 ? NS * 64 : (1 << 30));
+  if (NS > 0 && g.k_split > NS * 64) return hipErrorInvalidValue;  // K too long for one slice per step bound
+  hipLaunchKernelGGL((k_bp_gemm_mfma<EPI, RB, CP, NS>), dim3((g.N + BN - 1) / BN, (g.P + BP - 1) / BP, splits),
+                     dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+
 template <typename WT, int EPI>
 hipError_t gemm(const GemmArgs& g0, const BatchBuffers& b, int n_cu, hipStream_t s) {
   GemmArgs g = g0;
   constexpr int BK = 128 / sizeof(WT);
+  if constexpr (sizeof(WT) == 2) {
+    // bf16 weights: matrix cores; 64 rows x 16 positions per workgroup for
+    // few positions (many short K-slices keep the weight stream in flight),
+    // else 128 rows x 64 positions
+    if (g.P <= 16) {
+      // few positions: narrow tiles, K split over the waves of a workgroup
+      // gate/up reuses each lane's activations for four row blocks
+      constexpr int RB = EPI == kEpiSwiGlu ? 4 : 1, NW = 8, PF = EPI == kEpiResid ? 8 : (RB > 1 ? 2 : 4);
+      hipLaunchKernelGGL((k_bp_gemm_narrow<EPI, RB, NW, PF>), dim3((g.N + 16 * RB - 1) / (16 * RB)), dim3(NW * 64),
+                         0, s, g);
+      return hipGetLastError();
+    }
+    return gemm_mfma<EPI, 2, 4, 0>(g, b, n_cu, 2, s);
+  }
   if (g.P <= 16) {
     // few positions: narrow tiles (16 positions x 64 rows, one position and
     // four rows per thread) so that few K-slices fill the device and the
@@ -744,7 +1177,14 @@ hipError_t attention(AttnArgs a, const BatchBuffers& b, int n_cu, hipStream_t s)
   ns = static_cast<int>(std::min<size_t>(ns, std::max<size_t>(1, b.attn_ws_floats / per)));
   a.keys_per_split = (key_tiles + ns - 1) / ns * kKT;
   a.nsplit = (t_max + a.keys_per_split - 1) / a.keys_per_split;
-  hipLaunchKernelGGL((k_bp_attn<WT, D>), dim3(a.K * nqt * a.nsplit), dim3(256), 0, s, a);
+  const dim3 grid(a.K * nqt * a.nsplit);
+  switch (a.G) {
+#define EE_ATTN_G(GG) \
+  case GG: hipLaunchKernelGGL((k_bp_attn<WT, D, GG>), grid, dim3(256), 0, s, a); break;
+    EE_ATTN_G(1) EE_ATTN_G(2) EE_ATTN_G(3) EE_ATTN_G(4) EE_ATTN_G(5) EE_ATTN_G(6) EE_ATTN_G(7) EE_ATTN_G(8)
+#undef EE_ATTN_G
+    default: return hipErrorInvalidValue;
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.nsplit == 1) return e;
   hipLaunchKernelGGL((k_bp_attn_merge<D>), dim3((a.P * a.A + 3) / 4), dim3(256), 0, s, a);
@@ -827,7 +1267,8 @@ hipError_t launch_batched_pass(const BatchPass& bp, int pos0, const int32_t* d_t
 }
 
 size_t batch_tile_counters(int max_positions, int N_max) {
-  // tiles of 64 x 64 (more than 16 positions) and 16 x 64 (at most 16)
+  // tiles of 64 x 64 (more than 16 positions) and 16 x 64 (at most 16); on
+  // the matrix cores 128 rows x 64 positions and 64 x 16
   const size_t a = static_cast<size_t>((N_max + 63) / 64) * ((max_positions + 63) / 64);
   const size_t b = static_cast<size_t>((N_max + 63) / 64);
   return std::max(a, b);
