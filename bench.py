@@ -147,7 +147,7 @@ def exit_rate_fit(results, exit_layer, steps):
             "slope_ratio_measured_to_model": float(slope / model_slope)}
 
 
-def cpu_baseline(cfg, w, prompt, tau, exit_layer, seconds, measure="maxprob"):
+def cpu_baseline(cfg, w, prompt, tau, exit_layer, seconds, measure="maxprob", prompt_len=PROMPT):
     """The CPU oracle (fp64 numpy) on a bounded sample of the same workload."""
     import numpy as np
     import oracle
@@ -156,7 +156,7 @@ def cpu_baseline(cfg, w, prompt, tau, exit_layer, seconds, measure="maxprob"):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = len(os.sched_getaffinity(0))
-    o = oracle.OracleDecoder(cfg, w, PROMPT + 256)
+    o = oracle.OracleDecoder(cfg, w, prompt_len + 256)
     log("cpu baseline: oracle built")
     t = time.perf_counter()
     tok = o.prefill(prompt)
@@ -176,7 +176,7 @@ def cpu_baseline(cfg, w, prompt, tau, exit_layer, seconds, measure="maxprob"):
         if (el >= seconds and n >= 4) or n >= 256:
             break
     return {"value": n / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": (f"fp64 numpy oracle: prefill of the {PROMPT}-token prompt "
+            "sample": (f"fp64 numpy oracle: prefill of the {prompt_len}-token prompt "
                        f"({prefill_s:.1f} s, untimed), then the first {n} gated decode steps "
                        f"at the headline tau (exit rate {exits / n:.2f}) on the host cores")}
 
@@ -271,6 +271,190 @@ def measure(e, cfg, w, Le, args):
 
 
 
+def timeline_fill_us(e, cfg, Le, n, prompt):
+    """Duration of the KV-absence fill phase of an exit step, from the device
+    timeline of workgroup 0 (an imposed always-exit launch of n steps: each
+    step runs 5 Le layer phases, the readout, its head and the fill)."""
+    import numpy as np
+    per = 5 * Le + 3
+    cap = 2 * (n * per + 2)
+    e.ee_reset()
+    e.ee_prefill(prompt)
+    e.ee_set_timeline(cap)
+    e.ee_decode_n_ex(math.inf, Le, n, force_exit=np.ones(n, np.int32))
+    kernel_ms = e.ee_last_decode_ms()
+    t = e.ee_read_timeline(cap).astype(np.int64)
+    e.ee_set_timeline(0)
+    # ticks per microsecond from the launch's own span against its HIP-event time
+    span = t[2 * (n * per) + 1] - t[2 * 1]
+    tpu = span / (kernel_ms * 1e3)
+    fills = [(t[2 * ((i + 1) * per) + 1] - t[2 * ((i + 1) * per)]) / tpu for i in range(n // 2, n)]
+    return float(np.median(fills)), kernel_ms * 1e3 / n
+
+
+def grid_main(args):
+    """Exit layer x target exit rate grid on the 1.5B shape: tau per cell from a
+    64-prompt seeded calibration set, 256-token prompt, 128 generated tokens;
+    the KV-absence fill is timed separately."""
+    import numpy as np
+    import torch
+    import synth
+    from paper_2609_14144_amd import EE_CAL_EXIT_RATE, Engine
+    cfg = synth.get_config("d1p5b_sweep")
+    P, GEN, NCAL = 256, 128, 64
+    w = synth.generate_weights(cfg)
+    e = Engine(cfg, P + GEN + 8)
+    cells, fills = [], {}
+    try:
+        e.ee_load_weights(w)
+        cal = [synth.prompts(cfg, 1000 + i, P) for i in range(NCAL)]
+        prompt = synth.prompts(cfg, 1, P)
+        e.ee_prefill(synth.prompts(cfg, 2, P))
+        e.ee_decode_n(0.5, 14, 8)  # warm the code path
+        for Le in (7, 14, 21):
+            for r in (0.1, 0.5, 0.9):
+                t = time.perf_counter()
+                tau = e.ee_calibrate_threshold(cal, GEN, Le, EE_CAL_EXIT_RATE, r)
+                c = run_condition(e, cfg, tau, Le, prompt, 0, GEN)
+                c["target_exit_rate"] = r
+                cells.append(c)
+                log(f"L_e {Le} r {r}: tau {tau:.4g} ({time.perf_counter() - t:.1f}s) {c}")
+            fill_us, exit_step_us = timeline_fill_us(e, cfg, Le, 32, prompt)
+            fb = run_condition(e, cfg, math.inf, Le, prompt, 0, 32, full_every=1)
+            fills[str(Le)] = {"fill_us": fill_us, "exit_step_us": exit_step_us,
+                              "fallback_step_us": fb["kernel_ms"] * 1e3 / 32,
+                              "fill_share_of_exit_step": fill_us / exit_step_us,
+                              "fill_bytes": (cfg.n_layers - Le) * 2 * cfg.n_kv_heads * cfg.head_dim * cfg.hidden * 2}
+            log(f"L_e {Le} fill: {fills[str(Le)]}")
+        head = next(c for c in cells if c["exit_layer"] == 14 and c["target_exit_rate"] == 0.5)
+        roofline = {"bound": "hbm", "achieved": head["achieved_GBs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": head["achieved_GBs"] / PEAK_HBM_GBS, "traffic": None, "kernel": "k_decode_persistent",
+                    "algorithmic_bytes_per_launch": head["algorithmic_bytes"], "launch_ms": head["kernel_ms"]}
+    finally:
+        torch.cuda.synchronize()
+        e.close()
+        torch.cuda.synchronize()
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, w, prompt, head["tau"], 14, args.cpu_seconds, prompt_len=P)
+    out = {
+        "metric": METRIC, "value": head["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": GEN,
+        "warmup": 0, "ms_per_step": head["ms_per_step"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16 weights, f32 accumulate",
+        "data": "synthetic (seeded random weights N(0,0.02) and uniform random prompts)",
+        "config": {"workload": (f"1.5B-shaped decoder, exit-layer x exit-rate grid: exit layers 7/14/21 x target "
+                                f"exit rates 0.1/0.5/0.9, tau per cell from {NCAL} seeded {P}-token calibration "
+                                f"prompts x {GEN} full-depth steps; {P}-token prompt, {GEN} generated tokens, "
+                                f"batch 1; value = the layer-14, rate-0.5 cell"),
+                   "prompt_tokens": P, "exit_layer": 14, "target_exit_rate": 0.5,
+                   "realised_exit_rate": head["realised_exit_rate"], "tau": head["tau"]},
+        "roofline": roofline, "cpu_baseline": cpu, "grid": cells, "fill": fills,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def markov_schedule(n, seed):
+    """Bursty exits: a seeded two-state chain, exit -> exit with probability
+    7/8 (mean burst 8), stay -> exit with probability 1/2; stationary exit
+    rate 0.8."""
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    state, out = 0, np.zeros(n, np.int32)
+    for i in range(n):
+        state = int(rng.random() < (7 / 8 if state else 0.5))
+        out[i] = state
+    return out
+
+
+def long_main(args):
+    """Long context on the 1.5B shape: 8192-token prompt, then 1024 decode
+    steps with bursty exits (rate 0.8, mean burst 8) at layer 14. The bursts
+    are imposed exit decisions (the gate still computes its confidence
+    against tau, set at the 99th percentile of natural confidences)."""
+    import numpy as np
+    import torch
+    import synth
+    from paper_2609_14144_amd import EE_CAL_EXIT_RATE, Engine
+    cfg = synth.get_config("d1p5b")
+    P, GEN, Le = 8192, 1024, 14
+    w = synth.generate_weights(cfg)
+    e = Engine(cfg, P + GEN + 8)
+    sched = markov_schedule(GEN, 5)
+    try:
+        e.ee_load_weights(w)
+        cal = [synth.prompts(cfg, 200 + i, 512) for i in range(8)]
+        tau = e.ee_calibrate_threshold(cal, 64, Le, EE_CAL_EXIT_RATE, 0.01)
+        log(f"tau at the 99th percentile of natural confidences: {tau:.4g}")
+        prompt = synth.prompts(cfg, 3, P)
+        runs, pms = [], []
+        for _ in range(3):
+            e.ee_reset()
+            e.ee_prefill(prompt)
+            pms.append(e.ee_last_decode_ms())
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            tok, ex, conf, _ = e.ee_decode_n_ex(tau, Le, GEN, force_exit=sched)
+            torch.cuda.synchronize()
+            runs.append((e.ee_last_decode_ms(), time.perf_counter() - t0, ex.copy()))
+            log(f"long run: prompt pass {pms[-1]:.1f} ms, decode {runs[-1][0]:.1f} ms, exit rate {ex.mean():.3f}")
+        k = sorted(range(3), key=lambda i: runs[i][0])[1]
+        kernel_ms, wall, ex = runs[k]
+        nbytes = sum(step_bytes(cfg, Le, P + i + 1, bool(ex[i]), True) for i in range(GEN))
+        gbs = nbytes / (kernel_ms * 1e-3) / 1e9
+    finally:
+        torch.cuda.synchronize()
+        e.close()
+        torch.cuda.synchronize()
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline_long(cfg, w, P, tau, Le, sched, args.cpu_seconds)
+    out = {
+        "metric": METRIC, "value": GEN / wall, "unit": "tokens/s", "n_gpus": 1, "steps": GEN, "warmup": 0,
+        "ms_per_step": 1e3 * wall / GEN, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16 weights, f32 accumulate",
+        "data": "synthetic (seeded random weights N(0,0.02) and uniform random prompts)",
+        "config": {"workload": (f"1.5B-shaped decoder, long context: {P}-token prompt, {GEN} decode steps, "
+                                f"readout at layer {Le}, bursty imposed exits (two-state chain, mean burst 8, "
+                                f"stationary rate 0.8), tau at the 99th percentile of natural confidences, batch 1"),
+                   "prompt_tokens": P, "exit_layer": Le, "target_exit_rate": 0.8,
+                   "realised_exit_rate": float(ex.mean()), "tau": float(tau), "exits": "imposed (force_exit)"},
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": gbs / PEAK_HBM_GBS, "traffic": None, "kernel": "k_decode_persistent",
+                     "algorithmic_bytes_per_launch": nbytes, "launch_ms": kernel_ms,
+                     "launch_ms_reps": [r[0] for r in runs]},
+        "cpu_baseline": cpu,
+        "prompt_pass": {"positions": P, "kernel_ms": sorted(pms)[1], "kernel_ms_reps": pms},
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline_long(cfg, w, P, tau, exit_layer, sched, seconds):
+    """The oracle's decode steps at the long context's length: its cache holds
+    P positions (zeros: the step's arithmetic does not depend on the cached
+    values, and the oracle's own prompt pass of 8192 positions takes minutes)."""
+    import oracle
+    threads = len(os.sched_getaffinity(0))
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [threads])
+    except Exception:
+        pass
+    o = oracle.OracleDecoder(cfg, w, P + 80)
+    o.pos = P
+    tok, n = 1, 0
+    t = time.perf_counter()
+    while True:
+        r = o.decode_step(tok, tau, exit_layer, int(sched[n]))
+        tok = r.token
+        n += 1
+        el = time.perf_counter() - t
+        if (el >= seconds and n >= 4) or n >= 64:
+            break
+    return {"value": n / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"fp64 numpy oracle: the first {n} decode steps of the long-context schedule at "
+                       f"{P} cached positions (cache zero-filled instead of the oracle's prompt pass), host cores")}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -288,6 +472,10 @@ def main():
                     help="KV-absence fill in the exit step, or deferred and batched")
     ap.add_argument("--confidence", choices=list(MEASURES), default="maxprob",
                     help="softmax confidence measure the gate compares with tau (Section 10)")
+    ap.add_argument("--workload", choices=["decode", "grid", "long"], default="decode",
+                    help="decode: the 1.5B decode step at target exit rates 0.5 (headline), 0 and 0.96; "
+                         "grid: exit layers 7/14/21 x target exit rates 0.1/0.5/0.9 (256-token prompts, "
+                         "128 generated); long: 8192-token prompt, 1024 steps with bursty exits at rate 0.8")
     ap.add_argument("--copy-probe", type=float, default=0.0, metavar="MIB",
                     help="first run one plain elementwise copy of MIB MiB (float32 neg), whose "
                          "profiler counters scale the decode kernel's byte counters")
@@ -307,6 +495,10 @@ def main():
     if not torch.cuda.is_available():
         log("no GPU visible")
         sys.exit(1)
+    if args.workload == "grid":
+        return grid_main(args)
+    if args.workload == "long":
+        return long_main(args)
     if args.copy_probe > 0:
         n = int(args.copy_probe * 2 ** 20) // 4
         x = torch.ones(n, device="cuda")

@@ -307,10 +307,13 @@ int ee_set_persistent_grid(ee_ctx* ctx, int32_t nwg);
 
 /* Diagnostic timeline of the persistent kernel (test hook): with capacity > 0,
  * later launches record the device wall clock (hipDeviceAttributeWallClockRate
- * ticks) at each grid barrier of workgroup 0 — entry 2e when it arrives at
- * barrier e (1-based within the launch), 2e+1 when its wait returns — up to
- * capacity entries. capacity 0 turns it off. ee_read_timeline copies the
- * first n entries of the latest launch into out (host). */
+ * ticks) in workgroup 0 around every phase of the launch — entry 2e when phase
+ * e (1-based: the phases of each step in order, five per layer, then the
+ * readout, its head, and the KV fill or the final head) has requested its
+ * weights and is about to wait for its input, 2e+1 when it has issued its
+ * outputs — up to capacity entries. capacity 0 turns it off.
+ * ee_read_timeline copies the first n entries of the latest launch into out
+ * (host). */
 int ee_set_timeline(ee_ctx* ctx, int32_t capacity);
 int ee_read_timeline(ee_ctx* ctx, uint64_t* out, int32_t n);
 

@@ -1737,8 +1737,6 @@ __device__ inline void bar_arrive(const DevParams& p, uint32_t& epoch, int wg, i
       if (o2 == ngroups * epoch - 1)
         __hip_atomic_store(&p.counters->gen[0], epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    if (p.timeline && wg == 0 && 2 * static_cast<int>(epoch) < p.timeline_cap)
-      p.timeline[2 * epoch] = wall_clock64();
   }
 }
 
@@ -1757,8 +1755,6 @@ __device__ inline void bar_wait(const DevParams& p, uint32_t epoch) {
       }
       __builtin_amdgcn_s_sleep(1);
     }
-    if (p.timeline && blockIdx.x == 0 && 2 * static_cast<int>(epoch) + 1 < p.timeline_cap)
-      p.timeline[2 * epoch + 1] = wall_clock64();
   }
   __syncthreads();
 }
