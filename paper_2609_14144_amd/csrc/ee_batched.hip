@@ -731,13 +731,15 @@ __global__ __launch_bounds__(256) void k_bp_gemm_mfma(GemmArgs g) {
 }
 
 // ---------------------------------------------------------------------------
-// Few positions (P <= 16) on the matrix cores without a cross-workgroup
-// merge: a workgroup owns RB x 16 weight rows and all 16 positions, its NW
-// waves split K into contiguous ranges of 64-wide steps, and the waves' sums
-// meet in LDS in wave order. Lane l (row / position l % 16, group l / 16)
-// loads its own operands straight into registers: 32 bytes of its weight
-// row, 16 activations of its position (and their gains), the same k range
-// k0 + 16 (l / 16) .. + 15 as above; a ring of PF steps is in flight.
+// Few positions (P <= 16) on the matrix cores: a workgroup owns RB x 16
+// weight rows and all 16 positions over one K-slice (blockIdx.y of
+// gridDim.y), its NW waves split the slice into contiguous ranges of 64-wide
+// steps, and the waves' sums meet in LDS in wave order. Lane l (row /
+// position l % 16, group l / 16) loads its own operands straight into
+// registers: 32 bytes of its weight row, 16 activations of its position (and
+// their gains), the same k range k0 + 16 (l / 16) .. + 15 as above; a ring of
+// PF steps is in flight. With several slices the last workgroup of a tile to
+// arrive adds the slices' sums (and sums of squares) in slice order.
 // ---------------------------------------------------------------------------
 template <int EPI, int RB, int NW, int PF>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_bp_gemm_narrow(GemmArgs g) {
@@ -748,7 +750,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int lg = lane >> 4, lr = lane & 15;
   const int n0 = blockIdx.x * 16 * RB;
-  const int nsteps = (g.K + KS - 1) / KS;
+  const int split = blockIdx.y, splits = gridDim.y;
+  const int kb = split * g.k_split, ke = min(g.K, kb + g.k_split);
+  const int nsteps = (ke - kb + KS - 1) / KS;
   const int s0 = nsteps * wave / NW, s1 = nsteps * (wave + 1) / NW;
   const bool pok = lr < g.P;
   const uint16_t* W = static_cast<const uint16_t*>(g.W);
@@ -758,17 +762,17 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   float4 xr[PF][4];
   float4 gr[kGain ? PF : 1][4];
   auto load = [&](int st, int slot) {
-    const int k = st * KS + 16 * lg;
+    const int k = kb + st * KS + 16 * lg;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       const int row = n0 + rb * 16 + lr;
       const uint4* src = reinterpret_cast<const uint4*>(W + static_cast<int64_t>(row) * g.K + k);
-      wr[slot][rb][0] = (row < g.N && k < g.K) ? src[0] : make_uint4(0u, 0u, 0u, 0u);
-      wr[slot][rb][1] = (row < g.N && k + 8 < g.K) ? src[1] : make_uint4(0u, 0u, 0u, 0u);
+      wr[slot][rb][0] = (row < g.N && k < ke) ? src[0] : make_uint4(0u, 0u, 0u, 0u);
+      wr[slot][rb][1] = (row < g.N && k + 8 < ke) ? src[1] : make_uint4(0u, 0u, 0u, 0u);
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const bool ok = k + 4 * q < g.K;
+      const bool ok = k + 4 * q < ke;
       xr[slot][q] = (pok && ok) ? *reinterpret_cast<const float4*>(xrow + k + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
       if constexpr (kGain)
         gr[slot][q] = ok ? *reinterpret_cast<const float4*>(g.gain + k + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -830,15 +834,69 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     for (int w = 1; w < NW; ++w) t += red[w][rb][lane];
     acc[rb] = t;
   }
-  float rinv = 1.f;
+  // position lr's sum of squares over the slice: the four lane groups of
+  // every wave
+  float t = 0.f;
   if constexpr (kGain) {
-    // position lr's sum of squares: the four lane groups of every wave
-    float t = 0.f;
 #pragma unroll
     for (int w = 0; w < NW; ++w)
       t += (ssr[w][lr] + ssr[w][lr + 16]) + (ssr[w][lr + 32] + ssr[w][lr + 48]);
-    rinv = rsqrtf(t / static_cast<float>(g.K) + g.eps);
   }
+  if (splits > 1) {
+    // lane's outputs: rows n0 + 16 rb + 4 lg + i (i < 4) of position lr
+    const int64_t PN = static_cast<int64_t>(g.P) * g.N;
+    if (pok) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const int n = n0 + rb * 16 + 4 * lg;
+        float* d = g.part + split * PN + static_cast<int64_t>(lr) * g.N + n;
+        if (n < g.N) st_agent2(d, acc[rb][0], acc[rb][1]);
+        if (n + 2 < g.N) st_agent2(d + 2, acc[rb][2], acc[rb][3]);
+      }
+      if (kGain && lg == 0) st_agent(g.part + splits * PN + split * g.P + lr, t);
+    }
+    drain_stores();
+    int last = 0;
+    if (lane == 0) {
+      uint32_t* ctr = g.tile_ctr + blockIdx.x;
+      const uint32_t old = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      last = old == static_cast<uint32_t>(splits - 1);
+      if (last) __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (!__builtin_amdgcn_readfirstlane(last)) return;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    t = 0.f;
+    constexpr int kSG = 4;  // slices with loads in flight together
+    for (int q0 = 0; q0 < splits; q0 += kSG) {
+      float2 v[kSG][RB][2];
+      float vs[kSG];
+#pragma unroll
+      for (int u = 0; u < kSG; ++u) {
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          const int n = n0 + rb * 16 + 4 * lg;
+          const float* d = g.part + (q0 + u) * PN + static_cast<int64_t>(lr) * g.N + n;
+          const bool ok = pok && q0 + u < splits;
+          v[u][rb][0] = (ok && n < g.N) ? ld_agent2(d) : make_float2(0.f, 0.f);
+          v[u][rb][1] = (ok && n + 2 < g.N) ? ld_agent2(d + 2) : make_float2(0.f, 0.f);
+        }
+        vs[u] = (kGain && pok && q0 + u < splits) ? ld_agent(g.part + splits * PN + (q0 + u) * g.P + lr) : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < kSG; ++u) {
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          acc[rb][0] += v[u][rb][0].x;
+          acc[rb][1] += v[u][rb][0].y;
+          acc[rb][2] += v[u][rb][1].x;
+          acc[rb][3] += v[u][rb][1].y;
+        }
+        t += vs[u];
+      }
+    }
+  }
+  const float rinv = kGain ? rsqrtf(t / static_cast<float>(g.K) + g.eps) : 1.f;
   if (!pok) return;
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
@@ -1132,11 +1190,21 @@ hipError_t gemm(const GemmArgs& g0, const BatchBuffers& b, int n_cu, hipStream_t
     // few positions (many short K-slices keep the weight stream in flight),
     // else 128 rows x 64 positions
     if (g.P <= 16) {
-      // few positions: narrow tiles, K split over the waves of a workgroup
-      // gate/up reuses each lane's activations for four row blocks
-      constexpr int RB = EPI == kEpiSwiGlu ? 4 : 1, NW = 8, PF = EPI == kEpiResid ? 8 : (RB > 1 ? 2 : 4);
-      hipLaunchKernelGGL((k_bp_gemm_narrow<EPI, RB, NW, PF>), dim3((g.N + 16 * RB - 1) / (16 * RB)), dim3(NW * 64),
-                         0, s, g);
+      // few positions: narrow tiles, K split over the four waves of a
+      // workgroup (two workgroups per unit) and, where the tiles alone leave
+      // units idle, over workgroups: tiles times slices stay within one
+      // round of the units' slots, with at least two steps per wave. Gate/up
+      // reuses each lane's activations for four row blocks, the others for
+      // two, which halves the activation reads of every row.
+      constexpr int RB = EPI == kEpiSwiGlu ? 4 : 2, NW = 4, PF = EPI == kEpiResid ? 4 : 2;
+      const int tiles = (g.N + 16 * RB - 1) / (16 * RB);
+      if (static_cast<size_t>(tiles) > b.n_tile_ctr) return hipErrorInvalidValue;
+      int splits = std::max(1, std::min(2 * n_cu / tiles, (g.K + 64 * 2 * NW - 1) / (64 * 2 * NW)));
+      const size_t per = static_cast<size_t>(g.P) * g.N + g.P;
+      splits = static_cast<int>(std::min<size_t>(splits, std::max<size_t>(1, b.gemm_ws_floats / per)));
+      g.k_split = ((g.K + splits - 1) / splits + 63) / 64 * 64;
+      splits = (g.K + g.k_split - 1) / g.k_split;
+      hipLaunchKernelGGL((k_bp_gemm_narrow<EPI, RB, NW, PF>), dim3(tiles, splits), dim3(NW * 64), 0, s, g);
       return hipGetLastError();
     }
     return gemm_mfma<EPI, 2, 4, 0>(g, b, n_cu, 2, s);
@@ -1268,9 +1336,10 @@ hipError_t launch_batched_pass(const BatchPass& bp, int pos0, const int32_t* d_t
 
 size_t batch_tile_counters(int max_positions, int N_max) {
   // tiles of 64 x 64 (more than 16 positions) and 16 x 64 (at most 16); on
-  // the matrix cores 128 rows x 64 positions and 64 x 16
+  // the matrix cores 128 rows x 64 positions and, for at most 16 positions,
+  // 32 rows (two row blocks) x 16
   const size_t a = static_cast<size_t>((N_max + 63) / 64) * ((max_positions + 63) / 64);
-  const size_t b = static_cast<size_t>((N_max + 63) / 64);
+  const size_t b = static_cast<size_t>((N_max + 31) / 32);
   return std::max(a, b);
 }
 
