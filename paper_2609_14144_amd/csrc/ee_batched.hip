@@ -35,6 +35,8 @@
 
 namespace ee {
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
 namespace {
 
 // ---------------------------------------------------------------------------
@@ -1000,19 +1002,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 
   for (int k0 = kb; k0 < ke; k0 += kKT) {
     if (k0 != kb) offsets(k0, off);
-    uint4 kv[CPT], vv[CPT];
+    // native vectors: a copy of the uint4 struct from global memory to LDS
+    // through registers compiles to memory-to-memory copies through private
+    // memory, which serialise the loads
+    u32x4 kv[CPT], vv[CPT];
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
-      kv[i] = *reinterpret_cast<const uint4*>(kp + off[i]);
-      vv[i] = *reinterpret_cast<const uint4*>(vp + off[i]);
+      kv[i] = *reinterpret_cast<const u32x4*>(kp + off[i]);
+      vv[i] = *reinterpret_cast<const u32x4*>(vp + off[i]);
     }
     __syncthreads();  // previous tile consumed (and Qs written before the first)
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
       const int c = tid + 256 * i;
       const int j = c / CPK, q = c - j * CPK;
-      Ks[j * KST + q] = kv[i];  // keys past ke repeat key ke - 1; their scores are masked
-      Vs[c] = vv[i];
+      *reinterpret_cast<u32x4*>(&Ks[j * KST + q]) = kv[i];  // keys past ke repeat key ke - 1; masked
+      *reinterpret_cast<u32x4*>(&Vs[c]) = vv[i];
     }
     __syncthreads();
     const int key = k0 + lane;
