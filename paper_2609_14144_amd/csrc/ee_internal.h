@@ -10,7 +10,9 @@ namespace ee {
 constexpr int kWG = 512;               // threads per workgroup, every kernel
 constexpr int kWaves = kWG / 64;       // 64-wide wavefronts per workgroup
 constexpr int kPosPerWave = 16;             // attention positions per wave
-constexpr int kAttnSplit = kWaves * kPosPerWave;  // positions per attention work item
+constexpr int kPosPerWaveLong = 32;         // ... from kLongAttnFrom positions on
+constexpr int kLongAttnFrom = 4096;
+constexpr int kAttnSplit = kWaves * kPosPerWave;  // positions per attention work item (the smaller)
 constexpr int kMaxGroup = 8;           // max query heads per KV head
 constexpr int kMaxHeadDim = 256;
 constexpr int kBarGroups = 8;          // first level of the grid barrier (one per XCD)

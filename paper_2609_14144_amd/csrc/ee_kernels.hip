@@ -652,8 +652,8 @@ __device__ void phase_qkv(const DevParams& p, int l, int pos, int step, int wg, 
 
 // ---------------------------------------------------------------------------
 // phase: decode attention over positions 0..pos, grouped-query. Workgroup
-// item = (kv head, pair of the query heads sharing it, split of kAttnSplit
-// positions); wave w of the item takes kPosPerWave positions. Lane (sub, dl)
+// item = (kv head, pair of the query heads sharing it, split of kWaves
+// attn_ppw(pos) positions); wave w of the item takes attn_ppw(pos) positions. Lane (sub, dl)
 // of a wave holds 16-byte chunk dl of K and V rows sub + PPW k (LPP lanes per
 // row, PPW rows per load, RPL rows per lane): a row's dot product with q is
 // summed over its LPP lanes with DPP, the softmax statistics over the wave's
@@ -680,10 +680,18 @@ __device__ void phase_qkv(const DevParams& p, int l, int pos, int step, int wg, 
 // vocabulary head's online softmax statistics.
 __device__ __forceinline__ float fexp(float x) { return __builtin_amdgcn_exp2f(x * 1.44269504088896341f); }
 
-__host__ __device__ inline int attn_nsplit(int pos) { return (pos + kAttnSplit) / kAttnSplit; }
+// Positions per wave of an item: kPosPerWave, or kPosPerWaveLong from
+// kLongAttnFrom positions on, where twice the positions per item keep the
+// items within one round of the workgroups and the merge within one LDS
+// chunk (at 8192 positions: 198 items instead of 390, 33 records instead of
+// 65). Every step picks it from its own position, identically in both
+// programs.
+__host__ __device__ inline int attn_ppw(int pos) { return pos >= kLongAttnFrom ? kPosPerWaveLong : kPosPerWave; }
+__host__ __device__ inline int attn_split(int pos) { return kWaves * attn_ppw(pos); }
+__host__ __device__ inline int attn_nsplit(int pos) { return (pos + attn_split(pos)) / attn_split(pos); }
 __host__ __device__ inline int attn_pairs(int G) { return (G + 1) >> 1; }
 __host__ __device__ inline int attn_wave_floats(int D) {
-  return 2 * kPosPerWave + 2 * D + 4;  // offsets | weighted V of 2 heads | m0 m1 l0 l1
+  return 2 * kPosPerWaveLong + 2 * D + 4;  // offsets | weighted V of 2 heads | m0 m1 l0 l1
 }
 __host__ __device__ inline int attn_lds_floats(int D) { return 2 * D + kWaves * attn_wave_floats(D); }
 __host__ __device__ inline int attn_rec_words(int D) { return 2 * D + 4; }  // partial record
@@ -754,13 +762,17 @@ __device__ __forceinline__ int attn_row_chunks(const DevParams& p) {
 
 // The K and V rows of one wave in registers; rows [0, nold) are positions
 // before pos, and when has_new, row nold is position pos.
-template <typename WT>
+// pw positions per wave (attn_ppw of the step, at most CAP): the row slots
+// past pw are neither loaded nor used. With CAP = kPosPerWave (steps below
+// kLongAttnFrom only) pw is that constant.
+template <typename WT, int CAP>
 struct AttnTask {
   static constexpr int N = Elem<WT>::N;
-  static constexpr int kRowsMax = kPosPerWave * 16 / 64;  // rows per lane at LPP = 16
+  static constexpr int kRowsMax = CAP * 16 / 64;  // rows per lane at LPP = 16
   uint4 kr[kRowsMax], vr[kRowsMax];
   uint4 knew, vnew;  // row nold, in the lanes of row group nold % PPW
   int nold;
+  int pw;
   bool has_new;
 
   __device__ __forceinline__ static int64_t* offw(const DevParams& p, float* lds) {
@@ -772,8 +784,8 @@ struct AttnTask {
     const int lane = threadIdx.x & 63;
     const int per_kvh = attn_pairs(p.G) * nsplit;
     const int kvh = it / per_kvh, sp = (it - kvh * per_kvh) % nsplit;
-    const int ws0 = sp * kAttnSplit + wave_id() * kPosPerWave;
-    if (lane < kPosPerWave && ws0 + lane <= pos) offw(p, lds)[lane] = kv_offset(p, l, ws0 + lane, kvh);
+    const int ws0 = sp * kWaves * pw + wave_id() * pw;
+    if (lane < pw && ws0 + lane <= pos) offw(p, lds)[lane] = kv_offset(p, l, ws0 + lane, kvh);
     __builtin_amdgcn_wave_barrier();
   }
   // Rows [0, n) into kr/vr. Slots of rows >= n load row n - 1 again (no
@@ -781,13 +793,14 @@ struct AttnTask {
   template <int LPP>
   __device__ __forceinline__ void load_old(const DevParams& p, const int64_t* ow, int n) {
     if (n <= 0) return;
-    constexpr int PPW = 64 / LPP, RPL = kPosPerWave / PPW;
+    constexpr int PPW = 64 / LPP, RPL = CAP / PPW;
     const int lane = threadIdx.x & 63;
     const int sub = lane / LPP, dl = lane - sub * LPP;
     const WT* kp = static_cast<const WT*>(p.kpool);
     const WT* vp = static_cast<const WT*>(p.vpool);
 #pragma unroll
     for (int k = 0; k < RPL; ++k) {
+      if (CAP > kPosPerWave && PPW * k >= pw) break;
       const int64_t o = ow[min(sub + PPW * k, n - 1)] + dl * N;
       kr[k] = *reinterpret_cast<const uint4*>(kp + o);
       vr[k] = *reinterpret_cast<const uint4*>(vp + o);
@@ -806,13 +819,14 @@ struct AttnTask {
   template <int LPP>
   __device__ __forceinline__ void prefetch(const DevParams& p, int l, int pos, int wg, int nwg, float* lds) {
     clear();
+    pw = CAP > kPosPerWave ? attn_ppw(pos) : kPosPerWave;
     const int nsplit = attn_nsplit(pos);
     const int it = nwg - 1 - wg;
     if (it >= p.K * attn_pairs(p.G) * nsplit) return;
-    const int ws0 = (it % nsplit) * kAttnSplit + wave_id() * kPosPerWave;
+    const int ws0 = (it % nsplit) * kWaves * pw + wave_id() * pw;
     offsets(p, l, pos, it, nsplit, lds);
-    nold = max(0, min(kPosPerWave, pos - ws0));
-    has_new = pos >= ws0 && pos < ws0 + kPosPerWave;
+    nold = max(0, min(pw, pos - ws0));
+    has_new = pos >= ws0 && pos < ws0 + pw;
     load_old<LPP>(p, offw(p, lds), nold);
   }
   // After the barrier: the row of position pos (first item only).
@@ -854,11 +868,12 @@ struct AttnTask {
   }
 };
 
-template <typename WT, int LPP>
+template <typename WT, int LPP, int CAP>
 __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, float* lds,
-                                          AttnTask<WT>& t, const Sync& sy) {
+                                          AttnTask<WT, CAP>& t, const Sync& sy) {
   constexpr int N = Elem<WT>::N;
-  constexpr int PPW = 64 / LPP, RPL = kPosPerWave / PPW;
+  constexpr int PPW = 64 / LPP, RPL = CAP / PPW;
+  const int PW = CAP > kPosPerWave ? t.pw : kPosPerWave;
   const int T = pos + 1;
   const int nsplit = attn_nsplit(pos);
   const int G = p.G, D = p.D, GP = attn_pairs(G);
@@ -870,12 +885,12 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
   const int WF = attn_wave_floats(D);
   float* qs = lds;  // [2][D] q of heads g0, g1 (unscaled)
   float* wb = lds + 2 * D + wave * WF;
-  float* accw = wb + 2 * kPosPerWave;  // [2][D]
+  float* accw = wb + 2 * kPosPerWaveLong;  // [2][D]
   float* mlw = accw + 2 * D;           // m0 m1 l0 l1
   __shared__ int last_flag;
 
-  const int ws0 = sp * kAttnSplit + wave * kPosPerWave;
-  const int wn = max(0, min(kPosPerWave, T - ws0));  // positions of this wave
+  const int ws0 = sp * kWaves * PW + wave * PW;
+  const int wn = max(0, min(PW, T - ws0));  // positions of this wave
   const int tid = threadIdx.x;
   __syncthreads();
   if (tid < 2 * D)
@@ -895,6 +910,7 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
     float ma = -INFINITY, mb = -INFINITY;
 #pragma unroll
     for (int k = 0; k < RPL; ++k) {
+      if (CAP > kPosPerWave && PPW * k >= PW) break;  // slots past the step's positions per wave
       uint4 kc = t.template krow<LPP>(k, sub);
       keep_packed(kc);
       float kf[N];
@@ -916,6 +932,7 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
     float la = 0.f, lb = 0.f;
 #pragma unroll
     for (int k = 0; k < RPL; ++k) {
+      if (CAP > kPosPerWave && PPW * k >= PW) break;
       sa[k] = fexp(sa[k] - ma);  // exp(-inf) = 0 for rows past the wave's end
       sb[k] = fexp(sb[k] - mb);
       la += sa[k];
@@ -928,6 +945,7 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
     for (int e = 0; e < N; ++e) aa[e] = ab[e] = 0.f;
 #pragma unroll
     for (int k = 0; k < RPL; ++k) {
+      if (CAP > kPosPerWave && PPW * k >= PW) break;
       uint4 vc = t.template vrow<LPP>(k, sub);
       keep_packed(vc);
       float vf[N];
@@ -963,18 +981,18 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
   const bool act = tid < 2 * D;
   const int hg = act ? tid / D : 0, dd = tid - hg * D;
   const bool dup = hg == 1 && g1 == g0;  // second head of an odd last pair
-  const int nw = min(kWaves, (T - sp * kAttnSplit + kPosPerWave - 1) / kPosPerWave);
+  const int nw = min(kWaves, (T - sp * kWaves * PW + PW - 1) / PW);
   float M = -INFINITY, den = 0.f, num = 0.f;
   {
     float mw[kWaves];
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) mw[w] = w < nw ? lds[2 * D + w * WF + 2 * kPosPerWave + 2 * D + hg] : -INFINITY;
+    for (int w = 0; w < kWaves; ++w) mw[w] = w < nw ? lds[2 * D + w * WF + 2 * kPosPerWaveLong + 2 * D + hg] : -INFINITY;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) M = fmaxf(M, mw[w]);
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
       if (w < nw) {
-        const float* wb2 = lds + 2 * D + w * WF + 2 * kPosPerWave;
+        const float* wb2 = lds + 2 * D + w * WF + 2 * kPosPerWaveLong;
         const float f = fexp(mw[w] - M);
         den = fmaf(f, wb2[2 * D + 2 + hg], den);
         num = fmaf(f, act ? wb2[tid] : 0.f, num);
@@ -1061,11 +1079,11 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
 }
 
 // The first item of the workgroup uses the rows t prefetched; further items
-// (more than one per workgroup only past nwg * kAttnSplit / K positions) load
-// theirs when they start.
-template <typename WT, int LPP>
+// (more than one per workgroup only when the items outnumber the workgroups)
+// load theirs when they start.
+template <typename WT, int LPP, int CAP>
 __device__ __forceinline__ void phase_attn(const DevParams& p, int l, int pos, int wg, int nwg,
-                                           float* lds, AttnTask<WT>& t, const Sync& sy) {
+                                           float* lds, AttnTask<WT, CAP>& t, const Sync& sy) {
   const int nsplit = attn_nsplit(pos);
   const int items = p.K * attn_pairs(p.G) * nsplit;
   const int first = nwg - 1 - wg;
@@ -1073,13 +1091,35 @@ __device__ __forceinline__ void phase_attn(const DevParams& p, int l, int pos, i
     if (it != first) {
       __syncthreads();  // offsets of the previous item may still be read
       t.offsets(p, l, pos, it, nsplit, lds);
-      const int ws0 = (it % nsplit) * kAttnSplit + wave_id() * kPosPerWave;
-      t.nold = max(0, min(kPosPerWave, pos - ws0));
-      t.has_new = pos >= ws0 && pos < ws0 + kPosPerWave;  // read from its tagged copy
-      t.template load_old<LPP>(p, AttnTask<WT>::offw(p, lds), t.nold);
+      const int pw = CAP > kPosPerWave ? t.pw : kPosPerWave;
+      const int ws0 = (it % nsplit) * kWaves * pw + wave_id() * pw;
+      t.nold = max(0, min(pw, pos - ws0));
+      t.has_new = pos >= ws0 && pos < ws0 + pw;  // read from its tagged copy
+      t.template load_old<LPP>(p, AttnTask<WT, CAP>::offw(p, lds), t.nold);
     }
-    attn_item<WT, LPP>(p, pos, it, lds, t, sy);
+    attn_item<WT, LPP, CAP>(p, pos, it, lds, t, sy);
   }
+}
+
+// The attention phase with the row layout (lanes per cache row); after the
+// prefetch, before the wait, `mark` runs (the timeline stamp of the
+// persistent program).
+template <typename WT, int LPP, int CAP, typename Mark>
+__device__ __forceinline__ void attn_run(const DevParams& p, int l, int pos, int wg, int nwg, float* lds,
+                                         const Sync& sy, Mark&& mark) {
+  AttnTask<WT, CAP> t;
+  t.template prefetch<LPP>(p, l, pos, wg, nwg, lds);
+  mark(0u);
+  phase_attn<WT, LPP, CAP>(p, l, pos, wg, nwg, lds, t, sy);
+}
+
+// CAP: the most positions per wave this program's steps use (kPosPerWave
+// when every step lies below kLongAttnFrom)
+template <typename WT, int CAP, typename Mark>
+__device__ __forceinline__ void attn_dispatch(const DevParams& p, int l, int pos, int wg, int nwg, float* lds,
+                                              const Sync& sy, Mark&& mark) {
+  if (attn_row_chunks<WT>(p) == 16) attn_run<WT, 16, CAP>(p, l, pos, wg, nwg, lds, sy, mark);
+  else attn_run<WT, 8, CAP>(p, l, pos, wg, nwg, lds, sy, mark);
 }
 
 // ---------------------------------------------------------------------------
@@ -1601,16 +1641,7 @@ __global__ __launch_bounds__(kWG) void k_op(DevParams p, int l, int pos, int ste
     t.prefetch(p, l, pos, wg);
     phase_qkv<WT, CPL>(p, l, pos, step, wg, nwg, s.xs, s.red, t, sy);
   }
-  if constexpr (OP == kOpAttn) {
-    AttnTask<WT> t;
-    if (attn_row_chunks<WT>(p) == 16) {
-      t.template prefetch<16>(p, l, pos, wg, nwg, s.xs);
-      phase_attn<WT, 16>(p, l, pos, wg, nwg, s.xs, t, sy);
-    } else {
-      t.template prefetch<8>(p, l, pos, wg, nwg, s.xs);
-      phase_attn<WT, 8>(p, l, pos, wg, nwg, s.xs, t, sy);
-    }
-  }
+  if constexpr (OP == kOpAttn) attn_dispatch<WT, kPosPerWaveLong>(p, l, pos, wg, nwg, s.xs, sy, [](uint32_t) {});
   if constexpr (OP == kOpWo) {
     const WT* W = static_cast<const WT*>(p.layers[l].wo);
     RowTask<WT, CPL> t;
@@ -1800,23 +1831,15 @@ EE_PHASE_FN run_qkv(const DevParams& p, int l, int pos, int step, float* smem, T
   if (l == 0) tg.h = E;
 }
 
-EE_PHASE_FN run_attn(const DevParams& p, int l, int pos, float* smem, Tags& tg) {
+template <typename WT, int CPL, int CAP>
+__device__ __forceinline__ void run_attn(const DevParams& p, int l, int pos, float* smem, Tags& tg) {
   const int wg = opaque_wg();
-  AttnTask<WT> t;
   // the prefetch writes row offsets into LDS, which waves of this workgroup
   // may still be reading as the projection phase's input
   __syncthreads();
   const uint32_t E = ++tg.ep;
   const Sync sy{true, tg.q, 0u, E, 0u};
-  if (attn_row_chunks<WT>(p) == 16) {
-    t.template prefetch<16>(p, l, pos, wg, gridDim.x, smem);
-    tl_mark(p, 2 * E);
-    phase_attn<WT, 16>(p, l, pos, wg, gridDim.x, smem, t, sy);
-  } else {
-    t.template prefetch<8>(p, l, pos, wg, gridDim.x, smem);
-    tl_mark(p, 2 * E);
-    phase_attn<WT, 8>(p, l, pos, wg, gridDim.x, smem, t, sy);
-  }
+  attn_dispatch<WT, CAP>(p, l, pos, wg, gridDim.x, smem, sy, [&](uint32_t) { tl_mark(p, 2 * E); });
   tl_mark(p, 2 * E + 1);
   tg.o = E;
 }
@@ -1909,11 +1932,11 @@ EE_PHASE_FN run_fill_batch(const DevParams& p, int np, const int* ppos, const ui
 }
 #undef EE_PHASE_FN
 
-template <typename WT, int CPL>
+template <typename WT, int CPL, int CAP>
 __device__ __forceinline__ void run_layer(const DevParams& p, int l, int pos, int step, float* smem,
                                           Tags& tg) {
   run_qkv<WT, CPL>(p, l, pos, step, smem, tg);
-  run_attn<WT, CPL>(p, l, pos, smem, tg);
+  run_attn<WT, CPL, CAP>(p, l, pos, smem, tg);
   GateUpTask<WT, CPL> gu;
   run_wo<WT, CPL>(p, l, smem, tg, gu);
   run_gateup<WT, CPL>(p, l, smem, tg, gu);
@@ -1937,7 +1960,9 @@ __constant__ DevParams c_params[kParamSlots];
 // together before the first layer above exit_layer runs (then a grid barrier
 // orders the new rows before that layer's attention reads them), when the
 // slots are full, and before the launch ends.
-template <typename WT, int CPL>
+// CAP: attention positions per wave the launch may use (kPosPerWave when
+// every position of the launch lies below kLongAttnFrom).
+template <typename WT, int CPL, int CAP>
 __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_decode_persistent(
     int slot, int pos0, int n, int prefill) {
   extern __shared__ float smem[];
@@ -1955,7 +1980,7 @@ __global__ __launch_bounds__(kWG) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const int pos = pos0 + i;
     int exited = 0;
     for (int l = 0; l < p.L; ++l) {
-      run_layer<WT, CPL>(p, l, pos, i, smem, tg);
+      run_layer<WT, CPL, CAP>(p, l, pos, i, smem, tg);
       if (l + 1 == Le) {
         run_readout<WT, CPL>(p, smem, tg, lazy ? npend : 0);
         run_head<WT, CPL>(p, 1, i, smem, tg);
@@ -2167,26 +2192,34 @@ hipError_t launch_head_eval(const DevParams& p, int wbf16, const float* d_x, int
   });
 }
 
-static const void* persistent_fn(int wbf16, int cpl) {
+template <int CAP>
+static const void* persistent_fn_cap(int wbf16, int cpl) {
   if (wbf16) {
     switch (cpl) {
-      case 1: return reinterpret_cast<const void*>(&k_decode_persistent<uint16_t, 1>);
-      case 2: return reinterpret_cast<const void*>(&k_decode_persistent<uint16_t, 2>);
-      case 3: return reinterpret_cast<const void*>(&k_decode_persistent<uint16_t, 3>);
-      case 4: return reinterpret_cast<const void*>(&k_decode_persistent<uint16_t, 4>);
+      case 1: return reinterpret_cast<const void*>(&k_decode_persistent<uint16_t, 1, CAP>);
+      case 2: return reinterpret_cast<const void*>(&k_decode_persistent<uint16_t, 2, CAP>);
+      case 3: return reinterpret_cast<const void*>(&k_decode_persistent<uint16_t, 3, CAP>);
+      case 4: return reinterpret_cast<const void*>(&k_decode_persistent<uint16_t, 4, CAP>);
     }
   } else {
     switch (cpl) {
-      case 1: return reinterpret_cast<const void*>(&k_decode_persistent<float, 1>);
-      case 2: return reinterpret_cast<const void*>(&k_decode_persistent<float, 2>);
+      case 1: return reinterpret_cast<const void*>(&k_decode_persistent<float, 1, CAP>);
+      case 2: return reinterpret_cast<const void*>(&k_decode_persistent<float, 2, CAP>);
     }
   }
   return nullptr;
 }
 
+// positions [pos0, end): the program whose attention items take as many
+// positions per wave as the launch's last position needs
+static const void* persistent_fn(int wbf16, int cpl, int end) {
+  return end > kLongAttnFrom ? persistent_fn_cap<kPosPerWaveLong>(wbf16, cpl)
+                             : persistent_fn_cap<kPosPerWave>(wbf16, cpl);
+}
+
 static hipError_t persistent(const PersistentLaunch& L, int pos0, int n, int prefill) {
   const DevParams& p = *L.params_host;
-  const void* fn = persistent_fn(L.wbf16, chunks_per_lane(p, L.wbf16));
+  const void* fn = persistent_fn(L.wbf16, chunks_per_lane(p, L.wbf16), pos0 + n);
   if (!fn || L.slot < 0 || L.slot >= kParamSlots) return hipErrorInvalidValue;
   hipError_t e = hipMemcpyToSymbolAsync(HIP_SYMBOL(c_params), L.params_host, sizeof(DevParams),
                                         sizeof(DevParams) * L.slot, hipMemcpyHostToDevice, L.stream);
@@ -2208,10 +2241,14 @@ hipError_t launch_prefill_persistent(const PersistentLaunch& L, int pos0, int n)
 }
 
 int persistent_max_wgs_per_cu(const DevParams& p, int wbf16, size_t lds) {
-  int nb = 0;
-  const void* fn = persistent_fn(wbf16, chunks_per_lane(p, wbf16));
-  if (!fn || hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, kWG, lds) != hipSuccess) return 0;
-  return nb;
+  // both programs: the grid must fit either
+  int nb = 0, nl = 0;
+  const void* fn = persistent_fn_cap<kPosPerWave>(wbf16, chunks_per_lane(p, wbf16));
+  const void* fl = persistent_fn_cap<kPosPerWaveLong>(wbf16, chunks_per_lane(p, wbf16));
+  if (!fn || !fl || hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, kWG, lds) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&nl, fl, kWG, lds) != hipSuccess)
+    return 0;
+  return nb < nl ? nb : nl;
 }
 
 }  // namespace ee

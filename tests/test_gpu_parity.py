@@ -612,11 +612,14 @@ def test_calibration_matches_oracle():
     assert e.ee_position() == 0
 
 
-def test_long_context_attention():
-    """4000-position prompt: 63 attention splits per kv head, ragged tail."""
+@pytest.mark.parametrize("P", [4000, 8000])
+def test_long_context_attention(P):
+    """Long prompts at the tiny shape, ragged tails. 4000 positions: 32
+    attention splits of 16 positions per wave, 8000: 32 splits of 32 positions
+    per wave (the items from 4096 positions on); both more records than the
+    30 that the tiny shape's merge stages in LDS at once."""
     name = "tiny_bf16"
     cfg = synth.get_config(name)
-    P = 4000
     prompt = synth.prompts(cfg, 9, P)
     o = oracle_for(name, P + 4)
     g0 = o.prefill(prompt)
@@ -765,10 +768,9 @@ def test_other_model_shapes_lockstep(name):
 
 @pytest.mark.timeout(900)
 def test_d1p5b_long_prompt_lockstep():
-    """The 1.5B shape past 4352 positions: a 4608-token prompt gives 37
-    attention splits, more than the 34 partial records the merge stages in
-    LDS at once, so the last split merges in two chunks. Eight steps in
-    lockstep with the oracle with imposed branches, the prompt's cache
+    """The 1.5B shape past 4352 positions: a 4608-token prompt, whose steps
+    run the attention items of 32 positions per wave (19 splits). Eight steps
+    in lockstep with the oracle with imposed branches, the prompt's cache
     entries at the last layer, and the exited steps' filled entries."""
     cfg = synth.get_config(D15)
     P = 4608
