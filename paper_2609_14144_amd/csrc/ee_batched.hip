@@ -60,6 +60,24 @@ __device__ __forceinline__ float2 ld_agent2(const float* p) {
 }
 __device__ __forceinline__ void drain_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Bounds-checked 16-byte loads without a branch: an out-of-range lane reads
+// from `safe` (any valid address) and its bits are masked to zero where the
+// value is consumed. A load inside a conditional, or selected against zero,
+// is compiled to a branch around the load, and the branch's join waits for
+// every outstanding load; masking at the load itself waits for the load
+// there. Either would serialise a ring of prefetches.
+template <typename T>
+__device__ __forceinline__ T ld_clamped(const T* p, const T* safe, bool ok) {
+  return *(ok ? p : safe);
+}
+template <typename T>
+__device__ __forceinline__ T zero_unless(T v, bool ok) {
+  static_assert(sizeof(T) == 16, "16-byte values");
+  u32x4 u = __builtin_bit_cast(u32x4, v);
+  u &= ok ? 0xffffffffu : 0u;
+  return __builtin_bit_cast(T, u);
+}
+
 __device__ __forceinline__ float exp_hw(float x) { return __builtin_amdgcn_exp2f(x * 1.44269504088896341f); }
 
 template <typename WT>
@@ -743,61 +761,99 @@ __global__ __launch_bounds__(256) void k_bp_gemm_mfma(GemmArgs g) {
 // PF steps is in flight. With several slices the last workgroup of a tile to
 // arrive adds the slices' sums (and sums of squares) in slice order.
 // ---------------------------------------------------------------------------
+constexpr int kNarrowGainMax = 4096;  // longest K-slice of a normalised product on narrow tiles
+
 template <int EPI, int RB, int NW, int PF>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_bp_gemm_narrow(GemmArgs g) {
   constexpr int KS = 64;
   constexpr bool kGain = EPI != kEpiResid;  // the gated products normalise their input
+  constexpr int kGQ = kNarrowGainMax / (4 * NW * 64);  // gain float4s per thread
   __shared__ f32x4 red[NW][RB][64];
   __shared__ float ssr[NW][64];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  __shared__ float4 gs[kGain ? kNarrowGainMax / 4 : 1];  // the slice's RMSNorm gains
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lg = lane >> 4, lr = lane & 15;
   const int n0 = blockIdx.x * 16 * RB;
   const int split = blockIdx.y, splits = gridDim.y;
   const int kb = split * g.k_split, ke = min(g.K, kb + g.k_split);
   const int nsteps = (ke - kb + KS - 1) / KS;
   const int s0 = nsteps * wave / NW, s1 = nsteps * (wave + 1) / NW;
+  // every wave runs the same number of ring turns (steps at or past s1
+  // read a valid address and are masked to zero), so that the loop body
+  // has no branch: a branch around a load makes its join wait for every
+  // outstanding load
+  const int turns = ((nsteps + NW - 1) / NW + PF - 1) / PF;
   const bool pok = lr < g.P;
   const uint16_t* W = static_cast<const uint16_t*>(g.W);
   const float* xrow = g.A + static_cast<int64_t>(lr) * g.K;
 
+  // the slice's gains go through LDS (they are the same for every row and
+  // position); their loads are issued ahead of the weight ring's
+  float4 gl[kGain ? kGQ : 1];
+  if constexpr (kGain) {
+    const float4* g4 = reinterpret_cast<const float4*>(g.gain + kb);
+#pragma unroll
+    for (int j = 0; j < kGQ; ++j) {
+      const int c = tid + NW * 64 * j;
+      gl[j] = ld_clamped(g4 + c, g4, 4 * c < ke - kb);
+    }
+    // issued before the weight loads (the vector-memory counter is in
+    // order), so their LDS copy below waits for them alone
+    asm volatile("" ::: "memory");
+  }
   uint4 wr[PF][RB][2];
   float4 xr[PF][4];
-  float4 gr[kGain ? PF : 1][4];
+  // loads of step st into ring slot `slot`, out-of-range parts masked when
+  // the slot is consumed
   auto load = [&](int st, int slot) {
+    const bool sok = st < s1;
     const int k = kb + st * KS + 16 * lg;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       const int row = n0 + rb * 16 + lr;
       const uint4* src = reinterpret_cast<const uint4*>(W + static_cast<int64_t>(row) * g.K + k);
-      wr[slot][rb][0] = (row < g.N && k < ke) ? src[0] : make_uint4(0u, 0u, 0u, 0u);
-      wr[slot][rb][1] = (row < g.N && k + 8 < ke) ? src[1] : make_uint4(0u, 0u, 0u, 0u);
+      const uint4* w0 = reinterpret_cast<const uint4*>(W);
+      wr[slot][rb][0] = ld_clamped(src, w0, sok && row < g.N && k < ke);
+      wr[slot][rb][1] = ld_clamped(src + 1, w0, sok && row < g.N && k + 8 < ke);
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const bool ok = k + 4 * q < ke;
-      xr[slot][q] = (pok && ok) ? *reinterpret_cast<const float4*>(xrow + k + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
-      if constexpr (kGain)
-        gr[slot][q] = ok ? *reinterpret_cast<const float4*>(g.gain + k + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
+    for (int q = 0; q < 4; ++q)
+      xr[slot][q] = ld_clamped(reinterpret_cast<const float4*>(xrow + k + 4 * q),
+                               reinterpret_cast<const float4*>(g.A), sok && pok && k + 4 * q < ke);
   };
   f32x4 acc[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
   float ssq = 0.f;
 #pragma unroll
-  for (int i = 0; i < PF; ++i)
-    if (s0 + i < s1) load(s0 + i, i);
-  for (int st = s0; st < s1; st += PF) {
+  for (int i = 0; i < PF; ++i) load(s0 + i, i);
+  if constexpr (kGain) {
+    asm volatile("" ::: "memory");  // the ring's loads all issued first
+    static_assert(kGQ * NW * 64 * 4 == kNarrowGainMax, "gain staging covers the LDS copy");
+#pragma unroll
+    for (int j = 0; j < kGQ; ++j) {
+      const int c = tid + NW * 64 * j;
+      gs[c] = gl[j];  // past the slice: a valid gain, multiplying masked (zero) activations
+    }
+    __syncthreads();
+  }
+  for (int turn = 0; turn < turns; ++turn) {
+    const int st0 = s0 + turn * PF;
 #pragma unroll
     for (int i = 0; i < PF; ++i) {
-      if (st + i < s1) {
+      {
+        const int st = st0 + i;
+        const bool sok = st < s1;
+        const int k = kb + st * KS + 16 * lg;
         float4 x[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          x[q] = xr[i][q];
+          x[q] = zero_unless(xr[i][q], sok && pok && k + 4 * q < ke);
           if constexpr (kGain) {
+            const float4 gq = gs[min((k - kb) / 4 + q, kNarrowGainMax / 4 - 1)];
             ssq = fmaf(x[q].x, x[q].x, fmaf(x[q].y, x[q].y, fmaf(x[q].z, x[q].z, fmaf(x[q].w, x[q].w, ssq))));
-            x[q].x *= gr[i][q].x; x[q].y *= gr[i][q].y; x[q].z *= gr[i][q].z; x[q].w *= gr[i][q].w;
+            x[q].x *= gq.x; x[q].y *= gq.y; x[q].z *= gq.z; x[q].w *= gq.w;
           }
         }
         // three bf16 terms of the low (k .. k + 7) and high (k + 8 .. + 15) halves
@@ -807,10 +863,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
         uint4 wc[RB][2];
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
-          wc[rb][0] = wr[i][rb][0];
-          wc[rb][1] = wr[i][rb][1];
+          const bool rok = n0 + rb * 16 + lr < g.N;
+          wc[rb][0] = zero_unless(wr[i][rb][0], sok && rok && k < ke);
+          wc[rb][1] = zero_unless(wr[i][rb][1], sok && rok && k + 8 < ke);
         }
-        if (st + i + PF < s1) load(st + i + PF, i);  // refill the slot just read
+        load(st + PF, i);  // refill the slot just read
 #pragma unroll
         for (int term = 0; term < 3; ++term) {
           const uint4 blo = make_uint4(t[0][term].x, t[0][term].y, t[1][term].x, t[1][term].y);
@@ -1186,6 +1243,40 @@ hipError_t gemm_mfma(GemmArgs g, const BatchBuffers& b, int n_cu, int wgs_per_cu
   return hipGetLastError();
 }
 
+// Narrow tiles for at most 16 positions: RB x 16 rows by NW waves, which
+// split each K-slice into contiguous ranges of 64-wide steps. K is split over
+// workgroups where the tiles alone leave units idle: tiles times slices stay
+// within one round of the units' slots (eight waves per unit), with at least
+// two steps per wave.
+struct NarrowPlan {
+  int tiles, splits, k_split;
+  int64_t busiest;  // bytes the busiest unit loads (bf16 weights and 16 fp32 activation rows)
+};
+NarrowPlan narrow_plan(int EPI, int RB, int NW, const GemmArgs& g, size_t ws_floats, int n_cu) {
+  NarrowPlan q;
+  q.tiles = (g.N + 16 * RB - 1) / (16 * RB);
+  const int slots = n_cu * (8 / NW);
+  int splits = std::max(1, std::min(slots / q.tiles, (g.K + 64 * 2 * NW - 1) / (64 * 2 * NW)));
+  if (EPI != kEpiResid) splits = std::max(splits, (g.K + kNarrowGainMax - 1) / kNarrowGainMax);
+  const size_t per = static_cast<size_t>(g.P) * g.N + g.P;
+  splits = static_cast<int>(std::min<size_t>(splits, std::max<size_t>(1, ws_floats / per)));
+  q.k_split = ((g.K + splits - 1) / splits + 63) / 64 * 64;
+  q.splits = (g.K + q.k_split - 1) / q.k_split;
+  const int64_t wgs = static_cast<int64_t>(q.tiles) * q.splits;
+  q.busiest = (wgs + n_cu - 1) / n_cu * static_cast<int64_t>(q.k_split) * (32 * RB + 64);
+  return q;
+}
+
+template <int EPI, int RB, int NW, int PF>
+hipError_t gemm_narrow(GemmArgs g, const BatchBuffers& b, int n_cu, hipStream_t s) {
+  const NarrowPlan q = narrow_plan(EPI, RB, NW, g, b.gemm_ws_floats, n_cu);
+  if (static_cast<size_t>(q.tiles) > b.n_tile_ctr) return hipErrorInvalidValue;
+  if (EPI != kEpiResid && q.k_split > kNarrowGainMax) return hipErrorInvalidValue;
+  g.k_split = q.k_split;
+  hipLaunchKernelGGL((k_bp_gemm_narrow<EPI, RB, NW, PF>), dim3(q.tiles, q.splits), dim3(NW * 64), 0, s, g);
+  return hipGetLastError();
+}
+
 template <typename WT, int EPI>
 hipError_t gemm(const GemmArgs& g0, const BatchBuffers& b, int n_cu, hipStream_t s) {
   GemmArgs g = g0;
@@ -1195,22 +1286,26 @@ hipError_t gemm(const GemmArgs& g0, const BatchBuffers& b, int n_cu, hipStream_t
     // few positions (many short K-slices keep the weight stream in flight),
     // else 128 rows x 64 positions
     if (g.P <= 16) {
-      // few positions: narrow tiles, K split over the four waves of a
-      // workgroup (two workgroups per unit) and, where the tiles alone leave
-      // units idle, over workgroups: tiles times slices stay within one
-      // round of the units' slots, with at least two steps per wave. Gate/up
-      // reuses each lane's activations for four row blocks, the others for
-      // two, which halves the activation reads of every row.
-      constexpr int RB = EPI == kEpiSwiGlu ? 4 : 2, NW = 4, PF = EPI == kEpiResid ? 4 : 2;
-      const int tiles = (g.N + 16 * RB - 1) / (16 * RB);
-      if (static_cast<size_t>(tiles) > b.n_tile_ctr) return hipErrorInvalidValue;
-      int splits = std::max(1, std::min(2 * n_cu / tiles, (g.K + 64 * 2 * NW - 1) / (64 * 2 * NW)));
-      const size_t per = static_cast<size_t>(g.P) * g.N + g.P;
-      splits = static_cast<int>(std::min<size_t>(splits, std::max<size_t>(1, b.gemm_ws_floats / per)));
-      g.k_split = ((g.K + splits - 1) / splits + 63) / 64 * 64;
-      splits = (g.K + g.k_split - 1) / g.k_split;
-      hipLaunchKernelGGL((k_bp_gemm_narrow<EPI, RB, NW, PF>), dim3(tiles, splits), dim3(NW * 64), 0, s, g);
-      return hipGetLastError();
+      // few positions: narrow tiles. Large tiles of eight waves (one
+      // workgroup per unit) keep most of a matrix in flight at once; small
+      // tiles of four waves (two per unit) balance the units where the large
+      // tiles would leave some with two. The K split fills the units.
+      if constexpr (EPI == kEpiSwiGlu) {
+        // 80-row tiles of eight waves, or 64-row tiles of four waves (two
+        // per unit): whichever leaves the busiest unit fewer bytes to load
+        const NarrowPlan a5 = narrow_plan(EPI, 5, 8, g, b.gemm_ws_floats, n_cu);
+        const NarrowPlan a4 = narrow_plan(EPI, 4, 4, g, b.gemm_ws_floats, n_cu);
+        if (a4.busiest < a5.busiest) return gemm_narrow<EPI, 4, 4, 2>(g, b, n_cu, s);
+        return gemm_narrow<EPI, 5, 8, 2>(g, b, n_cu, s);
+      } else if constexpr (EPI == kEpiResid) {
+        // 64-row tiles of eight waves or 32-row tiles of four, by the same rule
+        const NarrowPlan a4 = narrow_plan(EPI, 4, 8, g, b.gemm_ws_floats, n_cu);
+        const NarrowPlan a2 = narrow_plan(EPI, 2, 4, g, b.gemm_ws_floats, n_cu);
+        if (a4.busiest < a2.busiest) return gemm_narrow<EPI, 4, 8, 2>(g, b, n_cu, s);
+        return gemm_narrow<EPI, 2, 4, 2>(g, b, n_cu, s);
+      } else {
+        return gemm_narrow<EPI, 2, 4, 2>(g, b, n_cu, s);
+      }
     }
     return gemm_mfma<EPI, 2, 4, 0>(g, b, n_cu, 2, s);
   }
