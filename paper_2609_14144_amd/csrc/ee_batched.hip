@@ -968,8 +968,8 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 // ---------------------------------------------------------------------------
 // causal grouped-query attention of a chunk of queries (positions pos0 ..
 // pos0 + P - 1) over the cache. Block = (KV head, tile of 4 query
-// positions, key split); wave w takes query position 4 t + w with the G query
-// heads of the KV head; keys in tiles of 64 staged in LDS, lane j = key j of
+// positions, key split); its waves split the tile's queries and the KV
+// head's query heads; keys in tiles of 64 staged in LDS, lane j = key j of
 // the tile; online softmax per head. One split writes o directly; several
 // write partial records (weighted V, max, sum) merged in split order by
 // k_bp_attn_merge.
@@ -988,13 +988,22 @@ struct AttnArgs {
   float scale;
 };
 
-constexpr int kQT = 4;   // query positions per block (one per wave)
+constexpr int kQT = 4;   // query positions per block
 constexpr int kKT = 64;  // keys per LDS tile
 
-// At most two workgroups fit per compute unit by LDS, so each wave may hold
-// up to 256 registers (two waves per SIMD).
+// Query heads per wave for G query heads per KV head: two or three where G
+// divides evenly (the block then runs G / GW waves per query position), else
+// all G.
+__host__ __device__ constexpr int attn_gw(int G) { return G % 2 == 0 ? 2 : (G % 3 == 0 ? 3 : G); }
+
+// Block = (KV head, tile of kQT query positions, key split); wave w takes
+// query position w % kQT and the GW query heads (w / kQT) GW .. + GW - 1 of
+// the KV head, so that the G heads' dot products run on G / GW waves. The
+// first four waves stage each key tile in LDS.
 template <typename WT, int D, int G>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_bp_attn(AttnArgs a) {
+__global__ __launch_bounds__(64 * kQT * (G / attn_gw(G))) void k_bp_attn(AttnArgs a) {
+  constexpr int GW = attn_gw(G);
+  static_assert(G % GW == 0, "head groups cover the KV head's query heads");
   constexpr int EPC = St<WT>::N;
   constexpr int CPK = D / EPC;          // 16-byte chunks per cache row
   constexpr int DPL = D / 64;           // output dimensions per lane (1 or 2)
@@ -1005,19 +1014,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   __shared__ float Ps[kQT][G][kKT];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int qw = wave % kQT, h0 = (wave / kQT) * GW;
+  const bool loader = tid < 256;        // the threads that stage key tiles
   const int nqt = (a.P + kQT - 1) / kQT;
   const int item = blockIdx.x;
   const int kvh = item / (nqt * a.nsplit);
   const int rem = item - kvh * nqt * a.nsplit;
   const int qt = rem / a.nsplit, sp = rem - qt * a.nsplit;
-  const int qi = qt * kQT + wave;               // query index within the chunk
+  const int qi = qt * kQT + qw;                 // query index within the chunk
   const bool active = qi < a.P;
   const int qpos = a.pos0 + qi;                 // its position
   const int t_end = a.pos0 + min(a.P, (qt + 1) * kQT);  // keys needed by the tile: [0, t_end)
   const int kb = sp * a.keys_per_split;
   const int ke = min(t_end, kb + a.keys_per_split);
 
-  constexpr int CPT = kKT * CPK / 256;  // chunks of K (and of V) per thread per tile
+  constexpr int CPT = kKT * CPK / 256;  // chunks of K (and of V) per loading thread per tile
   // cache offsets of a tile's chunks (its page lookups)
   auto offsets = [&](int k0, int64_t (&off)[CPT]) {
 #pragma unroll
@@ -1028,27 +1039,27 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       off[i] = cache_off(a.block_table, a.page_shift, a.page_size, a.K, D, a.layer_base, key, kvh) + q * EPC;
     }
   };
-  // the wave's query rows (the G heads of this KV head) and the first tile's
-  // page lookups, every load in flight at once
+  // the wave's query rows (its GW heads) and the first tile's page lookups,
+  // every load in flight at once
   int64_t off[CPT];
-  if (kb < ke) offsets(kb, off);
+  if (loader && kb < ke) offsets(kb, off);
   {
-    constexpr int QPL = G * D / 64;
+    constexpr int QPL = GW * D / 64;
     float qv[QPL];
 #pragma unroll
     for (int u = 0; u < QPL; ++u) {
-      const int i = lane + 64 * u, h = i / D, d = i - h * D;
+      const int i = lane + 64 * u, h = h0 + i / D, d = i % D;
       qv[u] = active ? a.Q[static_cast<int64_t>(qi) * a.A * D + (kvh * G + h) * D + d] : 0.f;
     }
 #pragma unroll
     for (int u = 0; u < QPL; ++u) {
-      const int i = lane + 64 * u, h = i / D, d = i - h * D;
-      Qs[wave][h][d] = qv[u];
+      const int i = lane + 64 * u, h = h0 + i / D, d = i % D;
+      Qs[qw][h][d] = qv[u];
     }
   }
-  float m_run[G], l_run[G], acc[G][DPL];
+  float m_run[GW], l_run[GW], acc[GW][DPL];
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
+  for (int h = 0; h < GW; ++h) {
     m_run[h] = -INFINITY;
     l_run[h] = 0.f;
 #pragma unroll
@@ -1058,42 +1069,46 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   const WT* vp = static_cast<const WT*>(a.vpool);
 
   for (int k0 = kb; k0 < ke; k0 += kKT) {
-    if (k0 != kb) offsets(k0, off);
     // native vectors: a copy of the uint4 struct from global memory to LDS
     // through registers compiles to memory-to-memory copies through private
     // memory, which serialise the loads
     u32x4 kv[CPT], vv[CPT];
+    if (loader) {
+      if (k0 != kb) offsets(k0, off);
 #pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      kv[i] = *reinterpret_cast<const u32x4*>(kp + off[i]);
-      vv[i] = *reinterpret_cast<const u32x4*>(vp + off[i]);
+      for (int i = 0; i < CPT; ++i) {
+        kv[i] = *reinterpret_cast<const u32x4*>(kp + off[i]);
+        vv[i] = *reinterpret_cast<const u32x4*>(vp + off[i]);
+      }
     }
     __syncthreads();  // previous tile consumed (and Qs written before the first)
+    if (loader) {
 #pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + 256 * i;
-      const int j = c / CPK, q = c - j * CPK;
-      *reinterpret_cast<u32x4*>(&Ks[j * KST + q]) = kv[i];  // keys past ke repeat key ke - 1; masked
-      *reinterpret_cast<u32x4*>(&Vs[c]) = vv[i];
+      for (int i = 0; i < CPT; ++i) {
+        const int c = tid + 256 * i;
+        const int j = c / CPK, q = c - j * CPK;
+        *reinterpret_cast<u32x4*>(&Ks[j * KST + q]) = kv[i];  // keys past ke repeat key ke - 1; masked
+        *reinterpret_cast<u32x4*>(&Vs[c]) = vv[i];
+      }
     }
     __syncthreads();
     const int key = k0 + lane;
     const bool valid = active && key < ke && key <= qpos;
-    float s[G];
+    float s[GW];
 #pragma unroll
-    for (int h = 0; h < G; ++h) s[h] = 0.f;
+    for (int h = 0; h < GW; ++h) s[h] = 0.f;
 #pragma unroll 2
     for (int q = 0; q < CPK; ++q) {
       float kf[EPC];
       St<WT>::unpack(Ks[lane * KST + q], kf);
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
+      for (int h = 0; h < GW; ++h) {
 #pragma unroll
-        for (int e = 0; e < EPC; ++e) s[h] = fmaf(Qs[wave][h][q * EPC + e], kf[e], s[h]);
+        for (int e = 0; e < EPC; ++e) s[h] = fmaf(Qs[qw][h0 + h][q * EPC + e], kf[e], s[h]);
       }
     }
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
+    for (int h = 0; h < GW; ++h) {
       const float sv = valid ? s[h] * a.scale : -INFINITY;
       const float mt = wave_max64(sv);
       const float mn = fmaxf(m_run[h], mt);
@@ -1106,7 +1121,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       m_run[h] = mn;
 #pragma unroll
       for (int e = 0; e < DPL; ++e) acc[h][e] *= alpha;
-      Ps[wave][h][lane] = p;
+      Ps[qw][h0 + h][lane] = p;
     }
     __builtin_amdgcn_wave_barrier();
     // weighted values: lane owns dimensions DPL * lane .. + DPL - 1
@@ -1114,17 +1129,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     for (int j = 0; j < kKT; ++j) {
       float v[DPL];
       if constexpr (DPL == 2) {
-        const float2 vv = St<WT>::load_pair(reinterpret_cast<const WT*>(&Vs[j * CPK]) + 2 * lane);
-        v[0] = vv.x;
-        v[1] = vv.y;
+        const float2 vv2 = St<WT>::load_pair(reinterpret_cast<const WT*>(&Vs[j * CPK]) + 2 * lane);
+        v[0] = vv2.x;
+        v[1] = vv2.y;
       } else {
         const WT* vr = reinterpret_cast<const WT*>(&Vs[j * CPK]);
         if constexpr (sizeof(WT) == 2) v[0] = __uint_as_float(static_cast<uint32_t>(vr[lane]) << 16);
         else v[0] = vr[lane];
       }
 #pragma unroll
-      for (int h = 0; h < G; ++h) {
-        const float pj = Ps[wave][h][j];
+      for (int h = 0; h < GW; ++h) {
+        const float pj = Ps[qw][h0 + h][j];
 #pragma unroll
         for (int e = 0; e < DPL; ++e) acc[h][e] = fmaf(pj, v[e], acc[h][e]);
       }
@@ -1132,8 +1147,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   }
   if (!active) return;
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
-    const int head = kvh * G + h;
+  for (int h = 0; h < GW; ++h) {
+    const int head = kvh * G + h0 + h;
     if (a.nsplit == 1) {
       const float inv = 1.f / l_run[h];
 #pragma unroll
@@ -1348,7 +1363,7 @@ hipError_t attention(AttnArgs a, const BatchBuffers& b, int n_cu, hipStream_t s)
   const dim3 grid(a.K * nqt * a.nsplit);
   switch (a.G) {
 #define EE_ATTN_G(GG) \
-  case GG: hipLaunchKernelGGL((k_bp_attn<WT, D, GG>), grid, dim3(256), 0, s, a); break;
+  case GG: hipLaunchKernelGGL((k_bp_attn<WT, D, GG>), grid, dim3(64 * kQT * (GG / attn_gw(GG))), 0, s, a); break;
     EE_ATTN_G(1) EE_ATTN_G(2) EE_ATTN_G(3) EE_ATTN_G(4) EE_ATTN_G(5) EE_ATTN_G(6) EE_ATTN_G(7) EE_ATTN_G(8)
 #undef EE_ATTN_G
     default: return hipErrorInvalidValue;
