@@ -881,17 +881,32 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
       }
     }
   }
+  // The tile's outputs in units of two: unit u = (row block u / 2, half
+  // u % 2 of each lane's four rows), lane (lg, lr) holding rows
+  // n0 + 16 (u / 2) + 4 lg + 2 (u % 2) + {0, 1} of position lr. Wave w sums
+  // units w, w + NW, ... over the waves' partial products (in wave order)
+  // and, with several K-slices, stores them, and the last workgroup of the
+  // tile to arrive merges every slice of every unit with all of its loads in
+  // flight at once.
+  constexpr int NU = 2 * RB, UPW = (NU + NW - 1) / NW;
+  __shared__ int last_flag;
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) red[wave][rb][lane] = acc[rb];
   ssr[wave][lane] = ssq;
   __syncthreads();
-  if (wave != 0) return;
+  float2 y[UPW];
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    f32x4 t = red[0][rb][lane];
+  for (int j = 0; j < UPW; ++j) {
+    const int u = wave + NW * j;
+    y[j] = make_float2(0.f, 0.f);
+    if (u < NU) {
+      const int rb = u >> 1, c = 2 * (u & 1);
 #pragma unroll
-    for (int w = 1; w < NW; ++w) t += red[w][rb][lane];
-    acc[rb] = t;
+      for (int w = 0; w < NW; ++w) {
+        y[j].x += red[w][rb][lane][c];
+        y[j].y += red[w][rb][lane][c + 1];
+      }
+    }
   }
   // position lr's sum of squares over the slice: the four lane groups of
   // every wave
@@ -901,67 +916,71 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
     for (int w = 0; w < NW; ++w)
       t += (ssr[w][lr] + ssr[w][lr + 16]) + (ssr[w][lr + 32] + ssr[w][lr + 48]);
   }
-  if (splits > 1) {
-    // lane's outputs: rows n0 + 16 rb + 4 lg + i (i < 4) of position lr
-    const int64_t PN = static_cast<int64_t>(g.P) * g.N;
-    if (pok) {
+  auto unit_n = [&](int j) { const int u = wave + NW * j; return n0 + 16 * (u >> 1) + 4 * lg + 2 * (u & 1); };
+  auto unit_ok = [&](int j) { return wave + NW * j < NU && unit_n(j) < g.N && pok; };
+  // the residual rows the epilogue adds to, requested before any wait
+  float2 xold[EPI == kEpiResid ? UPW : 1];
+  if constexpr (EPI == kEpiResid) {
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        const int n = n0 + rb * 16 + 4 * lg;
-        float* d = g.part + split * PN + static_cast<int64_t>(lr) * g.N + n;
-        if (n < g.N) st_agent2(d, acc[rb][0], acc[rb][1]);
-        if (n + 2 < g.N) st_agent2(d + 2, acc[rb][2], acc[rb][3]);
-      }
-      if (kGain && lg == 0) st_agent(g.part + splits * PN + split * g.P + lr, t);
+    for (int j = 0; j < UPW; ++j) {
+      const float2* xp = reinterpret_cast<const float2*>(g.Y + static_cast<int64_t>(lr) * g.N + unit_n(j));
+      xold[j] = unit_ok(j) ? *xp : make_float2(0.f, 0.f);
     }
+  }
+  if (splits > 1) {
+    const int64_t PN = static_cast<int64_t>(g.P) * g.N;
+#pragma unroll
+    for (int j = 0; j < UPW; ++j)
+      if (unit_ok(j)) st_agent2(g.part + split * PN + static_cast<int64_t>(lr) * g.N + unit_n(j), y[j].x, y[j].y);
+    if (kGain && wave == 0 && lg == 0 && pok) st_agent(g.part + splits * PN + split * g.P + lr, t);
     drain_stores();
-    int last = 0;
-    if (lane == 0) {
+    __syncthreads();  // every wave's partial sums stored
+    if (tid == 0) {
       uint32_t* ctr = g.tile_ctr + blockIdx.x;
       const uint32_t old = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      last = old == static_cast<uint32_t>(splits - 1);
-      if (last) __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      last_flag = old == static_cast<uint32_t>(splits - 1);
+      if (last_flag) __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    if (!__builtin_amdgcn_readfirstlane(last)) return;
+    __syncthreads();
+    if (!last_flag) return;
+    constexpr int kSG = 16;  // slices with loads in flight together
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < UPW; ++j) y[j] = make_float2(0.f, 0.f);
     t = 0.f;
-    constexpr int kSG = 4;  // slices with loads in flight together
     for (int q0 = 0; q0 < splits; q0 += kSG) {
-      float2 v[kSG][RB][2];
+      float2 v[UPW][kSG];
       float vs[kSG];
 #pragma unroll
       for (int u = 0; u < kSG; ++u) {
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          const int n = n0 + rb * 16 + 4 * lg;
-          const float* d = g.part + (q0 + u) * PN + static_cast<int64_t>(lr) * g.N + n;
-          const bool ok = pok && q0 + u < splits;
-          v[u][rb][0] = (ok && n < g.N) ? ld_agent2(d) : make_float2(0.f, 0.f);
-          v[u][rb][1] = (ok && n + 2 < g.N) ? ld_agent2(d + 2) : make_float2(0.f, 0.f);
+        for (int j = 0; j < UPW; ++j) {
+          const float* d = g.part + (q0 + u) * PN + static_cast<int64_t>(lr) * g.N + unit_n(j);
+          v[j][u] = (unit_ok(j) && q0 + u < splits) ? ld_agent2(d) : make_float2(0.f, 0.f);
         }
         vs[u] = (kGain && pok && q0 + u < splits) ? ld_agent(g.part + splits * PN + (q0 + u) * g.P + lr) : 0.f;
       }
 #pragma unroll
       for (int u = 0; u < kSG; ++u) {
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          acc[rb][0] += v[u][rb][0].x;
-          acc[rb][1] += v[u][rb][0].y;
-          acc[rb][2] += v[u][rb][1].x;
-          acc[rb][3] += v[u][rb][1].y;
+        for (int j = 0; j < UPW; ++j) {
+          y[j].x += v[j][u].x;
+          y[j].y += v[j][u].y;
         }
         t += vs[u];
       }
     }
   }
   const float rinv = kGain ? rsqrtf(t / static_cast<float>(g.K) + g.eps) : 1.f;
-  if (!pok) return;
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int n = n0 + rb * 16 + 4 * lg;
-    if (n < g.N) epi_pair<uint16_t>(g, EPI, lr, n, acc[rb][0] * rinv, acc[rb][1] * rinv);
-    if (n + 2 < g.N) epi_pair<uint16_t>(g, EPI, lr, n + 2, acc[rb][2] * rinv, acc[rb][3] * rinv);
+  for (int j = 0; j < UPW; ++j) {
+    if (!unit_ok(j)) continue;
+    const int n = unit_n(j);
+    if constexpr (EPI == kEpiResid) {
+      *reinterpret_cast<float2*>(g.Y + static_cast<int64_t>(lr) * g.N + n) =
+          make_float2(xold[j].x + y[j].x, xold[j].y + y[j].y);
+    } else {
+      epi_pair<uint16_t>(g, EPI, lr, n, y[j].x * rinv, y[j].y * rinv);
+    }
   }
 }
 
