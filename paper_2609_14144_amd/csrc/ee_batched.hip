@@ -1010,18 +1010,23 @@ struct AttnArgs {
 constexpr int kQT = 4;   // query positions per block
 constexpr int kKT = 64;  // keys per LDS tile
 
-// Query heads per wave for G query heads per KV head: two or three where G
-// divides evenly (the block then runs G / GW waves per query position), else
-// all G.
+// Query heads per wave for G query heads per KV head when the blocks are few
+// (a refresh): two or three where G divides evenly (the block then runs
+// G / GW waves per query position), else all G. With many blocks (a prompt)
+// every wave takes all G heads: more waves would read each key tile from LDS
+// once per wave.
 __host__ __device__ constexpr int attn_gw(int G) { return G % 2 == 0 ? 2 : (G % 3 == 0 ? 3 : G); }
 
 // Block = (KV head, tile of kQT query positions, key split); wave w takes
 // query position w % kQT and the GW query heads (w / kQT) GW .. + GW - 1 of
 // the KV head, so that the G heads' dot products run on G / GW waves. The
 // first four waves stage each key tile in LDS.
-template <typename WT, int D, int G>
-__global__ __launch_bounds__(64 * kQT * (G / attn_gw(G))) void k_bp_attn(AttnArgs a) {
-  constexpr int GW = attn_gw(G);
+// One wave per query position: at most two workgroups per compute unit (as
+// LDS allows), so each wave may hold up to 256 registers; G / GW waves per
+// position: that many per SIMD.
+template <typename WT, int D, int G, int GW>
+__global__ __launch_bounds__(64 * kQT * (G / GW))
+__attribute__((amdgpu_waves_per_eu(G / GW > 1 ? G / GW : 2, G / GW > 1 ? G / GW : 2))) void k_bp_attn(AttnArgs a) {
   static_assert(G % GW == 0, "head groups cover the KV head's query heads");
   constexpr int EPC = St<WT>::N;
   constexpr int CPK = D / EPC;          // 16-byte chunks per cache row
@@ -1032,9 +1037,10 @@ __global__ __launch_bounds__(64 * kQT * (G / attn_gw(G))) void k_bp_attn(AttnArg
   __shared__ float Qs[kQT][G][D];
   __shared__ float Ps[kQT][G][kKT];
 
+  constexpr int HG = G / GW;            // waves per query position
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int qw = wave % kQT, h0 = (wave / kQT) * GW;
-  const bool loader = tid < 256;        // the threads that stage key tiles
+  const int qw = HG > 1 ? wave % kQT : wave, h0 = HG > 1 ? (wave / kQT) * GW : 0;
+  const bool loader = HG > 1 ? tid < 256 : true;  // the threads that stage key tiles
   const int nqt = (a.P + kQT - 1) / kQT;
   const int item = blockIdx.x;
   const int kvh = item / (nqt * a.nsplit);
@@ -1380,9 +1386,17 @@ hipError_t attention(AttnArgs a, const BatchBuffers& b, int n_cu, hipStream_t s)
   a.keys_per_split = (key_tiles + ns - 1) / ns * kKT;
   a.nsplit = (t_max + a.keys_per_split - 1) / a.keys_per_split;
   const dim3 grid(a.K * nqt * a.nsplit);
+  // few blocks: the heads split over waves; else one wave per query position
+  const bool split_heads = static_cast<int64_t>(grid.x) < 2 * n_cu;
   switch (a.G) {
-#define EE_ATTN_G(GG) \
-  case GG: hipLaunchKernelGGL((k_bp_attn<WT, D, GG>), grid, dim3(64 * kQT * (GG / attn_gw(GG))), 0, s, a); break;
+#define EE_ATTN_G(GG)                                                                                        \
+  case GG:                                                                                                   \
+    if (split_heads) {                                                                                       \
+      hipLaunchKernelGGL((k_bp_attn<WT, D, GG, attn_gw(GG)>), grid, dim3(64 * kQT * (GG / attn_gw(GG))), 0, s, a); \
+    } else {                                                                                                 \
+      hipLaunchKernelGGL((k_bp_attn<WT, D, GG, GG>), grid, dim3(64 * kQT), 0, s, a);                         \
+    }                                                                                                        \
+    break;
     EE_ATTN_G(1) EE_ATTN_G(2) EE_ATTN_G(3) EE_ATTN_G(4) EE_ATTN_G(5) EE_ATTN_G(6) EE_ATTN_G(7) EE_ATTN_G(8)
 #undef EE_ATTN_G
     default: return hipErrorInvalidValue;
