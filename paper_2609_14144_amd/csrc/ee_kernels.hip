@@ -1846,14 +1846,17 @@ __device__ __forceinline__ void run_attn(const DevParams& p, int l, int pos, flo
 
 // The gate/up tiles are requested here too, before the wait for the
 // attention output: most workgroups have no attention item and would leave
-// HBM idle while the attention workgroups finish.
-EE_PHASE_FN run_wo(const DevParams& p, int l, float* smem, Tags& tg, GateUpTask<WT, CPL>& gu) {
+// HBM idle while the attention workgroups finish. Not at long contexts
+// (early_gu false): there the attention's K and V rows are a large read of
+// their own, which the gate/up tiles would delay; they are requested when
+// the gate/up phase starts instead.
+EE_PHASE_FN run_wo(const DevParams& p, int l, float* smem, Tags& tg, GateUpTask<WT, CPL>& gu, bool early_gu) {
   const int wg = opaque_wg();
   const Lds s = lds_carve(p, smem);
   const WT* W = static_cast<const WT*>(p.layers[l].wo);
   RowTask<WT, CPL> t;
   t.prefetch(W, p.H, p.A * p.D, wg);
-  gu.prefetch(p, l, wg, gridDim.x);
+  if (early_gu) gu.prefetch(p, l, wg, gridDim.x);
   const uint32_t E = ++tg.ep;
   tl_mark(p, 2 * E);
   phase_rows<WT, CPL>(p, W, p.H, p.A * p.D, p.o, p.h, nullptr, 1, wg, gridDim.x, s.xs, t,
@@ -1862,9 +1865,10 @@ EE_PHASE_FN run_wo(const DevParams& p, int l, float* smem, Tags& tg, GateUpTask<
   tg.h = E;
 }
 
-EE_PHASE_FN run_gateup(const DevParams& p, int l, float* smem, Tags& tg, GateUpTask<WT, CPL>& t) {
+EE_PHASE_FN run_gateup(const DevParams& p, int l, float* smem, Tags& tg, GateUpTask<WT, CPL>& t, bool early_gu) {
   const int wg = opaque_wg();
   const Lds s = lds_carve(p, smem);
+  if (!early_gu) t.prefetch(p, l, wg, gridDim.x);
   const uint32_t E = ++tg.ep;
   tl_mark(p, 2 * E);
   phase_gateup<WT, CPL>(p, l, wg, gridDim.x, s.xs, s.red, t, Sync{true, tg.h, 0u, E, 0u});
@@ -1938,8 +1942,9 @@ __device__ __forceinline__ void run_layer(const DevParams& p, int l, int pos, in
   run_qkv<WT, CPL>(p, l, pos, step, smem, tg);
   run_attn<WT, CPL, CAP>(p, l, pos, smem, tg);
   GateUpTask<WT, CPL> gu;
-  run_wo<WT, CPL>(p, l, smem, tg, gu);
-  run_gateup<WT, CPL>(p, l, smem, tg, gu);
+  const bool early_gu = !(CAP > kPosPerWave && pos >= kLongAttnFrom);
+  run_wo<WT, CPL>(p, l, smem, tg, gu, early_gu);
+  run_gateup<WT, CPL>(p, l, smem, tg, gu, early_gu);
   run_down<WT, CPL>(p, l, smem, tg);
 }
 
