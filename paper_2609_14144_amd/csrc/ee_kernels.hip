@@ -244,6 +244,24 @@ __device__ inline void tw_stage(const DevParams& p, const uint64_t* src, int n, 
   }
 }
 
+// As tw_stage, for n words src[at(i)] (i < n) gathered into xs[0..n).
+template <int kB, typename At>
+__device__ inline void tw_gather(const DevParams& p, const uint64_t* src, int n, At at, uint32_t tag, bool poll,
+                                 float* xs) {
+  const uint64_t none = tw_pack(0.f, tag + 1u);
+  for (int base = 0; base < n; base += kB * kWG) {
+    uint64_t v[kB];
+#pragma unroll
+    for (int k = 0; k < kB; ++k) v[k] = base + k * kWG + static_cast<int>(threadIdx.x) < n ? none : tw_pack(0.f, tag);
+    EE_TW_POLL(kB, src + at(min(base + k * kWG + static_cast<int>(threadIdx.x), n - 1)), true)
+#pragma unroll
+    for (int k = 0; k < kB; ++k) {
+      const int i = base + k * kWG + static_cast<int>(threadIdx.x);
+      if (i < n) xs[i] = tw_val(v[k]);
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // reductions
 // ---------------------------------------------------------------------------
@@ -690,6 +708,7 @@ __host__ __device__ inline int attn_ppw(int pos) { return pos >= kLongAttnFrom ?
 __host__ __device__ inline int attn_split(int pos) { return kWaves * attn_ppw(pos); }
 __host__ __device__ inline int attn_nsplit(int pos) { return (pos + attn_split(pos)) / attn_split(pos); }
 __host__ __device__ inline int attn_pairs(int G) { return (G + 1) >> 1; }
+constexpr int kAttnMergers = 4;  // merging splits per head pair in the long-context program
 __host__ __device__ inline int attn_wave_floats(int D) {
   return 2 * kPosPerWaveLong + 2 * D + 4;  // offsets | weighted V of 2 heads | m0 m1 l0 l1
 }
@@ -1007,6 +1026,62 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
   // partial records, tagged: [K][GP][max_splits][2D weighted V | m0 m1 | l0 l1]
   const int RS = attn_rec_words(D);
   uint64_t* recs = p.attn_part + (static_cast<int64_t>(kvh) * GP + gp) * p.max_splits * RS;
+  const int cap = max(1, (lds_vec_floats(p) - 8) / (RS + 2));  // splits per merge chunk
+  if constexpr (CAP > kPosPerWave) {
+    // Many splits (the long-context program): every split publishes its
+    // record and the last kAttnMergers splits each merge one slice of the 2D
+    // elements, staging only that slice (and the head's max and sum) of every
+    // record; one merger staging whole records would wait on several rounds
+    // of loads. Same arithmetic, in the same chunks of splits, as the single
+    // merger below. Only when every item has a workgroup of its own: a
+    // merger here also waits for splits after its own, which in a second
+    // round of items could wait for it.
+    constexpr int MG = kAttnMergers;
+    const int E = 2 * D / MG;           // elements per merger (within one head)
+    const int RW = E + 2;               // staged words per record
+    if (sy.poll && nsplit >= 2 * MG && nsplit * RW + 4 <= lds_vec_floats(p) &&
+        p.K * GP * nsplit <= static_cast<int>(gridDim.x)) {
+      uint64_t* r = recs + static_cast<int64_t>(sp) * RS;
+      if (act) tw_store(r + tid, num, sy.tout);
+      if (act && dd == 0) {
+        tw_store(r + 2 * D + hg, M, sy.tout);
+        tw_store(r + 2 * D + 2 + hg, den, sy.tout);
+      }
+      const int mk = nsplit - 1 - sp;  // merger index
+      if (mk >= MG) return;
+      const int e0 = mk * E, mh = e0 / D;  // the slice's first element and its head
+      __syncthreads();  // LDS may still be read (wave records)
+      float* rl = lds;  // [nsplit][RW]: the slice's weighted V, then the head's max and sum
+      tw_gather<8>(p, recs, nsplit * RW, [&](int i) {
+        const int s2 = i / RW, j = i - s2 * RW;
+        return static_cast<int64_t>(s2) * RS + (j < E ? e0 + j : 2 * D + (j - E) * 2 + mh);
+      }, sy.tout, sy.poll, rl);
+      __syncthreads();
+      if (tid < E) {
+        const int e = e0 + tid, dm = e - mh * D;
+        float Mr = -INFINITY, Dr = 0.f, Nr = 0.f;
+        for (int c0 = 0; c0 < nsplit; c0 += cap) {
+          const int ns = min(cap, nsplit - c0);
+          float cm = Mr;
+          for (int s2 = 0; s2 < ns; ++s2) cm = fmaxf(cm, rl[(c0 + s2) * RW + E]);
+          const float sc = fexp(Mr - cm);
+          float dn = Dr * sc;
+          Nr *= sc;
+          for (int s2 = 0; s2 < ns; ++s2) {
+            const float* rr = rl + (c0 + s2) * RW;
+            const float f = fexp(rr[E] - cm);
+            dn = fmaf(f, rr[E + 1], dn);
+            Nr = fmaf(f, rr[tid], Nr);
+          }
+          Mr = cm;
+          Dr = dn;
+        }
+        const bool dup_m = mh == 1 && g1 == g0;
+        if (!dup_m) tw_store(p.o + (kvh * G + g0 + mh) * D + dm, Nr * (1.f / Dr), sy.tout);
+      }
+      return;
+    }
+  }
   const bool merger = sy.poll && sp == nsplit - 1;
   if (!merger) {
     uint64_t* r = recs + static_cast<int64_t>(sp) * RS;
@@ -1032,7 +1107,6 @@ __device__ __forceinline__ void attn_item(const DevParams& p, int pos, int it, f
   // into its slot instead of reading it back, so both programs do the same
   // arithmetic in the same order.
   float Mr = -INFINITY, Dr = 0.f, Nr = 0.f;
-  const int cap = max(1, (lds_vec_floats(p) - 8) / (RS + 2));
   float* rl = lds;                 // [cap][RS]
   float* wts = lds + cap * RS;     // [cap][2] split weights
   float* hsc = wts + 2 * cap;      // [2] rescale of the running values, then [2] 1 / sum
