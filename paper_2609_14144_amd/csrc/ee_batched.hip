@@ -756,10 +756,11 @@ __global__ __launch_bounds__(256) void k_bp_gemm_mfma(GemmArgs g) {
 // gridDim.y), its NW waves split the slice into contiguous ranges of 64-wide
 // steps, and the waves' sums meet in LDS in wave order. Lane l (row /
 // position l % 16, group l / 16) loads its own operands straight into
-// registers: 32 bytes of its weight row, 16 activations of its position (and
-// their gains), the same k range k0 + 16 (l / 16) .. + 15 as above; a ring of
-// PF steps is in flight. With several slices the last workgroup of a tile to
-// arrive adds the slices' sums (and sums of squares) in slice order.
+// registers: 32 bytes of its weight row and 16 activations of its position,
+// the same k range k0 + 16 (l / 16) .. + 15 as above (the slice's RMSNorm
+// gains come from LDS); a ring of PF steps is in flight. With several slices
+// the last workgroup of a tile to arrive adds the slices' sums (and sums of
+// squares) in slice order.
 // ---------------------------------------------------------------------------
 constexpr int kNarrowGainMax = 4096;  // longest K-slice of a normalised product on narrow tiles
 
