@@ -1008,27 +1008,23 @@ struct AttnArgs {
   float scale;
 };
 
-constexpr int kQT = 4;   // query positions per block
 constexpr int kKT = 64;  // keys per LDS tile
 
-// Query heads per wave for G query heads per KV head when the blocks are few
-// (a refresh): two or three where G divides evenly (the block then runs
-// G / GW waves per query position), else all G. With many blocks (a prompt)
-// every wave takes all G heads: more waves would read each key tile from LDS
-// once per wave.
-__host__ __device__ constexpr int attn_gw(int G) { return G % 2 == 0 ? 2 : (G % 3 == 0 ? 3 : G); }
-
-// Block = (KV head, tile of kQT query positions, key split); wave w takes
-// query position w % kQT and the GW query heads (w / kQT) GW .. + GW - 1 of
-// the KV head, so that the G heads' dot products run on G / GW waves. The
-// first four waves stage each key tile in LDS.
-// One wave per query position: at most two workgroups per compute unit (as
-// LDS allows), so each wave may hold up to 256 registers; G / GW waves per
-// position: that many per SIMD.
-template <typename WT, int D, int G, int GW>
-__global__ __launch_bounds__(64 * kQT * (G / GW))
-__attribute__((amdgpu_waves_per_eu(G / GW > 1 ? G / GW : 2, G / GW > 1 ? G / GW : 2))) void k_bp_attn(AttnArgs a) {
+// Block = (KV head, tile of QT query positions, key split); wave w takes
+// query position w % QT and the GW query heads (w / QT) GW .. + GW - 1 of the
+// KV head. With many blocks (a prompt) QT = 4 and each wave takes all G heads
+// (more waves would read each key tile from LDS once per wave), at most two
+// workgroups per compute unit (as LDS allows), so each wave may hold up to
+// 256 registers; with few blocks (a refresh) QT = 2 and one head per wave,
+// so that the G heads' dot products run on G waves per position. The first
+// four waves stage each key tile in LDS.
+template <typename WT, int D, int G, int GW, int QT>
+__global__ __launch_bounds__(64 * QT * (G / GW))
+__attribute__((amdgpu_waves_per_eu((QT * (G / GW) + 3) / 4 > 2 ? (QT * (G / GW) + 3) / 4 : 2,
+                                   (QT * (G / GW) + 3) / 4 > 2 ? (QT * (G / GW) + 3) / 4 : 2))) void k_bp_attn(AttnArgs a) {
   static_assert(G % GW == 0, "head groups cover the KV head's query heads");
+  static_assert(QT * (G / GW) >= 4, "four waves stage the key tiles");
+  constexpr int kQT = QT;
   constexpr int EPC = St<WT>::N;
   constexpr int CPK = D / EPC;          // 16-byte chunks per cache row
   constexpr int DPL = D / 64;           // output dimensions per lane (1 or 2)
@@ -1377,6 +1373,7 @@ hipError_t gemm(const GemmArgs& g0, const BatchBuffers& b, int n_cu, hipStream_t
 
 template <typename WT, int D>
 hipError_t attention(AttnArgs a, const BatchBuffers& b, int n_cu, hipStream_t s) {
+  constexpr int kQT = 4;  // query positions per block of the prompt's path
   const int nqt = (a.P + kQT - 1) / kQT;
   const int t_max = a.pos0 + a.P;
   const int key_tiles = (t_max + kKT - 1) / kKT;
@@ -1386,17 +1383,18 @@ hipError_t attention(AttnArgs a, const BatchBuffers& b, int n_cu, hipStream_t s)
   ns = static_cast<int>(std::min<size_t>(ns, std::max<size_t>(1, b.attn_ws_floats / per)));
   a.keys_per_split = (key_tiles + ns - 1) / ns * kKT;
   a.nsplit = (t_max + a.keys_per_split - 1) / a.keys_per_split;
-  const dim3 grid(a.K * nqt * a.nsplit);
-  // few blocks: the heads split over waves; else one wave per query position
-  const bool split_heads = static_cast<int64_t>(grid.x) < 2 * n_cu;
+  // few blocks: blocks of two query positions whose waves take one query
+  // head each; else four positions, one wave each with all heads
+  const bool split_heads = static_cast<int64_t>(a.K) * nqt * a.nsplit < 2 * n_cu && a.G >= 2;
+  const dim3 grid(a.K * (split_heads ? (a.P + 1) / 2 : nqt) * a.nsplit);
   switch (a.G) {
-#define EE_ATTN_G(GG)                                                                                        \
-  case GG:                                                                                                   \
-    if (split_heads) {                                                                                       \
-      hipLaunchKernelGGL((k_bp_attn<WT, D, GG, attn_gw(GG)>), grid, dim3(64 * kQT * (GG / attn_gw(GG))), 0, s, a); \
-    } else {                                                                                                 \
-      hipLaunchKernelGGL((k_bp_attn<WT, D, GG, GG>), grid, dim3(64 * kQT), 0, s, a);                         \
-    }                                                                                                        \
+#define EE_ATTN_G(GG)                                                                                  \
+  case GG:                                                                                             \
+    if (GG >= 2 && split_heads) {                                                                      \
+      hipLaunchKernelGGL((k_bp_attn<WT, D, GG, 1, (GG >= 2 ? 2 : 4)>), grid, dim3(128 * GG), 0, s, a); \
+    } else {                                                                                           \
+      hipLaunchKernelGGL((k_bp_attn<WT, D, GG, GG, 4>), grid, dim3(64 * kQT), 0, s, a);                \
+    }                                                                                                  \
     break;
     EE_ATTN_G(1) EE_ATTN_G(2) EE_ATTN_G(3) EE_ATTN_G(4) EE_ATTN_G(5) EE_ATTN_G(6) EE_ATTN_G(7) EE_ATTN_G(8)
 #undef EE_ATTN_G
