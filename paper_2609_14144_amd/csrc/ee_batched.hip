@@ -1285,15 +1285,18 @@ hipError_t gemm_mfma(GemmArgs g, const BatchBuffers& b, int n_cu, int wgs_per_cu
 // workgroups where the tiles alone leave units idle: tiles times slices stay
 // within one round of the units' slots (eight waves per unit), with at least
 // two steps per wave.
+constexpr int64_t kSliceMergeBytes = 72 << 10;
+
 struct NarrowPlan {
   int tiles, splits, k_split;
   int64_t busiest;  // bytes the busiest unit loads (bf16 weights and 16 fp32 activation rows)
 };
-NarrowPlan narrow_plan(int EPI, int RB, int NW, const GemmArgs& g, size_t ws_floats, int n_cu) {
+NarrowPlan narrow_plan(int EPI, int RB, int NW, const GemmArgs& g, size_t ws_floats, int n_cu,
+                       bool whole_k = false) {
   NarrowPlan q;
   q.tiles = (g.N + 16 * RB - 1) / (16 * RB);
   const int slots = n_cu * (8 / NW);
-  int splits = std::max(1, std::min(slots / q.tiles, (g.K + 64 * 2 * NW - 1) / (64 * 2 * NW)));
+  int splits = whole_k ? 1 : std::max(1, std::min(slots / q.tiles, (g.K + 64 * 2 * NW - 1) / (64 * 2 * NW)));
   if (EPI != kEpiResid) splits = std::max(splits, (g.K + kNarrowGainMax - 1) / kNarrowGainMax);
   const size_t per = static_cast<size_t>(g.P) * g.N + g.P;
   splits = static_cast<int>(std::min<size_t>(splits, std::max<size_t>(1, ws_floats / per)));
@@ -1301,12 +1304,15 @@ NarrowPlan narrow_plan(int EPI, int RB, int NW, const GemmArgs& g, size_t ws_flo
   q.splits = (g.K + q.k_split - 1) / q.k_split;
   const int64_t wgs = static_cast<int64_t>(q.tiles) * q.splits;
   q.busiest = (wgs + n_cu - 1) / n_cu * static_cast<int64_t>(q.k_split) * (32 * RB + 64);
+  // a K-slice merge (partial stores, their drain, the arrival count, the
+  // slices' loads: ~3 us) costs about what a unit loads in that time
+  if (q.splits > 1) q.busiest += kSliceMergeBytes;
   return q;
 }
 
 template <int EPI, int RB, int NW, int PF>
-hipError_t gemm_narrow(GemmArgs g, const BatchBuffers& b, int n_cu, hipStream_t s) {
-  const NarrowPlan q = narrow_plan(EPI, RB, NW, g, b.gemm_ws_floats, n_cu);
+hipError_t gemm_narrow(GemmArgs g, const BatchBuffers& b, int n_cu, hipStream_t s, bool whole_k = false) {
+  const NarrowPlan q = narrow_plan(EPI, RB, NW, g, b.gemm_ws_floats, n_cu, whole_k);
   if (static_cast<size_t>(q.tiles) > b.n_tile_ctr) return hipErrorInvalidValue;
   if (EPI != kEpiResid && q.k_split > kNarrowGainMax) return hipErrorInvalidValue;
   g.k_split = q.k_split;
@@ -1341,6 +1347,11 @@ hipError_t gemm(const GemmArgs& g0, const BatchBuffers& b, int n_cu, hipStream_t
         if (a4.busiest < a2.busiest) return gemm_narrow<EPI, 4, 8, 2>(g, b, n_cu, s);
         return gemm_narrow<EPI, 2, 4, 2>(g, b, n_cu, s);
       } else {
+        // 32-row tiles of four waves, or 16-row tiles of eight waves over the
+        // whole K (no slice merge), by the same rule
+        const NarrowPlan a2 = narrow_plan(EPI, 2, 4, g, b.gemm_ws_floats, n_cu);
+        const NarrowPlan a1 = narrow_plan(EPI, 1, 8, g, b.gemm_ws_floats, n_cu, true);
+        if (a1.busiest < a2.busiest) return gemm_narrow<EPI, 1, 8, 2>(g, b, n_cu, s, true);
         return gemm_narrow<EPI, 2, 4, 2>(g, b, n_cu, s);
       }
     }
