@@ -1344,6 +1344,8 @@ hipError_t gemm(const GemmArgs& g0, const BatchBuffers& b, int n_cu, hipStream_t
         // 64-row tiles of eight waves or 32-row tiles of four, by the same rule
         const NarrowPlan a4 = narrow_plan(EPI, 4, 8, g, b.gemm_ws_floats, n_cu);
         const NarrowPlan a2 = narrow_plan(EPI, 2, 4, g, b.gemm_ws_floats, n_cu);
+        const NarrowPlan a1 = narrow_plan(EPI, 1, 8, g, b.gemm_ws_floats, n_cu, true);
+        if (a1.busiest < a2.busiest && a1.busiest < a4.busiest) return gemm_narrow<EPI, 1, 8, 2>(g, b, n_cu, s, true);
         if (a4.busiest < a2.busiest) return gemm_narrow<EPI, 4, 8, 2>(g, b, n_cu, s);
         return gemm_narrow<EPI, 2, 4, 2>(g, b, n_cu, s);
       } else {
