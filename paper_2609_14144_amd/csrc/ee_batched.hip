@@ -516,10 +516,14 @@ __device__ __forceinline__ void split3(const float4& x, uint2* t) {
   for (int k = 0; k < 3; ++k) t[k] = make_uint2(b[k][0] | (b[k][1] << 16), b[k][2] | (b[k][3] << 16));
 }
 
-// NS > 0: the K-slice has at most NS steps and all its loads are issued
-// before the first product (few positions: each step has little arithmetic
-// to hide a load behind); NS = 0: the next step's loads fly during a step.
-template <int EPI, int RB, int CP, int NS>
+// A ring of PF steps of weight and activation loads is in flight; bounds are
+// applied without branches (an out-of-range lane reads a valid address and
+// is masked where consumed: a branch around a load makes its join wait for
+// every outstanding load), and the K-slice's RMSNorm gains are staged in LDS
+// once (a gain load per step would be waited for together with the ring).
+constexpr int kWideGainMax = 2048;  // longest K-slice of a normalised product on wide tiles
+
+template <int EPI, int RB, int CP, int PF>
 __global__ __launch_bounds__(256) void k_bp_gemm_mfma(GemmArgs g) {
   constexpr int BN = 64 * RB, BP = 16 * CP, KS = 64;
   constexpr int XCH = BP * KS / 4 / 256;  // float4 of activations per thread per step
@@ -535,43 +539,55 @@ __global__ __launch_bounds__(256) void k_bp_gemm_mfma(GemmArgs g) {
   const int kb = split * g.k_split, ke = min(g.K, kb + g.k_split);
   const uint16_t* W = static_cast<const uint16_t*>(g.W);
 
+  constexpr int kGW = kWideGainMax / (4 * 256);  // gain float4s per thread
+  __shared__ float4 gsm[EPI != kEpiResid ? kWideGainMax / 4 : 1];
+  float4 gl[EPI != kEpiResid ? kGW : 1];
+  if constexpr (EPI != kEpiResid) {
+    const float4* g4 = reinterpret_cast<const float4*>(g.gain + kb);
+#pragma unroll
+    for (int j = 0; j < kGW; ++j) gl[j] = ld_clamped(g4 + tid + 256 * j, g4, 4 * (tid + 256 * j) < ke - kb);
+    asm volatile("" ::: "memory");  // issued before the ring's loads
+  }
   float ssq[XCH];
 #pragma unroll
   for (int i = 0; i < XCH; ++i) ssq[i] = 0.f;
-  float4 xr[XCH];
-  uint4 wr[RB][2];
-  auto load_w_into = [&](int k0, uint4 (&wr)[RB][2]) {
+  const int nsteps = (ke - kb + KS - 1) / KS;
+  uint4 wq[PF][RB][2];
+  float4 xq[PF][XCH];
+  // loads of step st into ring slot `slot` (masked when consumed)
+  auto load = [&](int st, int slot) {
+    const bool sok = st < nsteps;
+    const int k0 = kb + st * KS;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       const int n = n0 + (wave * RB + rb) * 16 + lr;
       const int k = k0 + 16 * lg;
       const uint4* src = reinterpret_cast<const uint4*>(W + static_cast<int64_t>(n) * g.K + k);
-      wr[rb][0] = (n < g.N && k < ke) ? src[0] : make_uint4(0u, 0u, 0u, 0u);
-      wr[rb][1] = (n < g.N && k + 8 < ke) ? src[1] : make_uint4(0u, 0u, 0u, 0u);
+      const uint4* w0 = reinterpret_cast<const uint4*>(W);
+      wq[slot][rb][0] = ld_clamped(src, w0, sok && n < g.N && k < ke);
+      wq[slot][rb][1] = ld_clamped(src + 1, w0, sok && n < g.N && k + 8 < ke);
     }
-  };
-  auto load_x_into = [&](int k0, float4 (&xr)[XCH]) {
 #pragma unroll
     for (int i = 0; i < XCH; ++i) {
       const int c = tid + 256 * i;
       const int p = c >> 4, k = k0 + 4 * (c & 15);
-      xr[i] = (p0 + p < g.P && k < ke)
-                  ? *reinterpret_cast<const float4*>(g.A + static_cast<int64_t>(p0 + p) * g.K + k)
-                  : make_float4(0.f, 0.f, 0.f, 0.f);
+      xq[slot][i] = ld_clamped(reinterpret_cast<const float4*>(g.A + static_cast<int64_t>(p0 + p) * g.K + k),
+                               reinterpret_cast<const float4*>(g.A), sok && p0 + p < g.P && k < ke);
     }
   };
-  auto store_x_from = [&](int buf, int k0, const float4 (&xr)[XCH]) {
+  // step st's activations of ring slot `slot`: masked, normalised, split into
+  // three bf16 terms in LDS buffer buf
+  auto store_x = [&](int buf, int st, int slot) {
+    const int k0 = kb + st * KS;
 #pragma unroll
     for (int i = 0; i < XCH; ++i) {
       const int c = tid + 256 * i;
       const int p = c >> 4, kq = c & 15, k = k0 + 4 * kq;
-      float4 a = xr[i];
-      if (g.gain) {
+      float4 a = zero_unless(xq[slot][i], p0 + p < g.P && k < ke);
+      if constexpr (EPI != kEpiResid) {
         ssq[i] = fmaf(a.x, a.x, fmaf(a.y, a.y, fmaf(a.z, a.z, fmaf(a.w, a.w, ssq[i]))));
-        if (k < ke) {
-          const float4 gg = *reinterpret_cast<const float4*>(g.gain + k);
-          a.x *= gg.x; a.y *= gg.y; a.z *= gg.z; a.w *= gg.w;
-        }
+        const float4 gg = gsm[min(k - kb, kWideGainMax - 4) / 4];
+        a.x *= gg.x; a.y *= gg.y; a.z *= gg.z; a.w *= gg.w;
       }
       uint2 t[3];
       split3(a, t);
@@ -606,45 +622,32 @@ __global__ __launch_bounds__(256) void k_bp_gemm_mfma(GemmArgs g) {
     }
   };
 
-  if constexpr (NS > 0) {
-    // the whole K-slice's loads first
-    const int nst = (ke - kb + KS - 1) / KS;
-    uint4 wall[NS][RB][2];
-    float4 xall[NS][XCH];
 #pragma unroll
-    for (int st = 0; st < NS; ++st) {
-      if (st < nst) {
-        load_w_into(kb + st * KS, wall[st]);
-        load_x_into(kb + st * KS, xall[st]);
-      }
-    }
+  for (int i = 0; i < PF; ++i) load(i, i);
+  if constexpr (EPI != kEpiResid) {
+    asm volatile("" ::: "memory");  // the ring's loads all issued first
+    static_assert(kGW * 256 * 4 == kWideGainMax, "gain staging covers the LDS copy");
 #pragma unroll
-    for (int st = 0; st < NS; ++st) {
-      if (st < nst) {
-        store_x_from(st & 1, kb + st * KS, xall[st]);
-        __syncthreads();
-        products(st & 1, wall[st]);
-      }
-    }
-  } else {
-    int buf = 0;
-    if (kb < ke) {
-      load_w_into(kb, wr);
-      load_x_into(kb, xr);
-    }
-    for (int k0 = kb; k0 < ke; k0 += KS) {
-      store_x_from(buf, k0, xr);
+    for (int j = 0; j < kGW; ++j) gsm[tid + 256 * j] = gl[j];  // past the slice: valid gains of masked activations
+    __syncthreads();
+  }
+  int buf = 0;
+  for (int st0 = 0; st0 < nsteps; st0 += PF) {
+#pragma unroll
+    for (int i = 0; i < PF; ++i) {
+      const int st = st0 + i;
+      if (st >= nsteps) break;  // the same for every wave
+      store_x(buf, st, i);
       __syncthreads();
+      const int k = kb + st * KS + 16 * lg;
       uint4 wc[RB][2];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
-        wc[rb][0] = wr[rb][0];
-        wc[rb][1] = wr[rb][1];
+        const bool rok = n0 + (wave * RB + rb) * 16 + lr < g.N;
+        wc[rb][0] = zero_unless(wq[i][rb][0], rok && k < ke);
+        wc[rb][1] = zero_unless(wq[i][rb][1], rok && k + 8 < ke);
       }
-      if (k0 + KS < ke) {  // the next step's loads fly during this step's products
-        load_w_into(k0 + KS, wr);
-        load_x_into(k0 + KS, xr);
-      }
+      load(st + PF, i);  // refill the slot just read
       products(buf, wc);
       buf ^= 1;  // the other buffer is written next; this one is read until the barrier after that store
     }
@@ -1266,16 +1269,16 @@ void choose_split(int tiles, int P, int N, int K, int BK, size_t ws_floats, int 
   *splits = (K + ks - 1) / ks;
 }
 
-template <int EPI, int RB, int CP, int NS>
+template <int EPI, int RB, int CP, int PF>
 hipError_t gemm_mfma(GemmArgs g, const BatchBuffers& b, int n_cu, int wgs_per_cu, hipStream_t s) {
   constexpr int BN = 64 * RB, BP = 16 * CP;
   const int tiles = ((g.N + BN - 1) / BN) * ((g.P + BP - 1) / BP);
   if (static_cast<size_t>(tiles) > b.n_tile_ctr) return hipErrorInvalidValue;
   int splits;
   choose_split(tiles, g.P, g.N, g.K, 64, b.gemm_ws_floats, wgs_per_cu, n_cu, &g.k_split, &splits,
-               NS > 0 ? NS * 64 : (1 << 30));
-  if (NS > 0 && g.k_split > NS * 64) return hipErrorInvalidValue;  // K too long for one slice per step bound
-  hipLaunchKernelGGL((k_bp_gemm_mfma<EPI, RB, CP, NS>), dim3((g.N + BN - 1) / BN, (g.P + BP - 1) / BP, splits),
+               EPI != kEpiResid ? kWideGainMax : (1 << 30));
+  if (EPI != kEpiResid && g.k_split > kWideGainMax) return hipErrorInvalidValue;  // gains staged in LDS
+  hipLaunchKernelGGL((k_bp_gemm_mfma<EPI, RB, CP, PF>), dim3((g.N + BN - 1) / BN, (g.P + BP - 1) / BP, splits),
                      dim3(256), 0, s, g);
   return hipGetLastError();
 }
@@ -1357,7 +1360,7 @@ hipError_t gemm(const GemmArgs& g0, const BatchBuffers& b, int n_cu, hipStream_t
         return gemm_narrow<EPI, 2, 4, 2>(g, b, n_cu, s);
       }
     }
-    return gemm_mfma<EPI, 2, 4, 0>(g, b, n_cu, 2, s);
+    return gemm_mfma<EPI, 2, 4, 3>(g, b, n_cu, 2, s);
   }
   if (g.P <= 16) {
     // few positions: narrow tiles (16 positions x 64 rows, one position and
