@@ -1021,9 +1021,10 @@ constexpr int kKT = 64;  // keys per LDS tile
 // 256 registers; with few blocks (a refresh) QT = 2 and one head per wave,
 // so that the G heads' dot products run on G waves per position. The first
 // four waves stage each key tile in LDS.
+// (fp32 caches of wide heads may need more registers: their lower bound is 1)
 template <typename WT, int D, int G, int GW, int QT>
 __global__ __launch_bounds__(64 * QT * (G / GW))
-__attribute__((amdgpu_waves_per_eu((QT * (G / GW) + 3) / 4 > 2 ? (QT * (G / GW) + 3) / 4 : 2,
+__attribute__((amdgpu_waves_per_eu(sizeof(WT) == 4 ? 1 : ((QT * (G / GW) + 3) / 4 > 2 ? (QT * (G / GW) + 3) / 4 : 2),
                                    (QT * (G / GW) + 3) / 4 > 2 ? (QT * (G / GW) + 3) / 4 : 2))) void k_bp_attn(AttnArgs a) {
   static_assert(G % GW == 0, "head groups cover the KV head's query heads");
   static_assert(QT * (G / GW) >= 4, "four waves stage the key tiles");
